@@ -1,0 +1,173 @@
+/*
+ * echo.h -- C ABI of the MI355X (gfx950) mixed paged-attention iteration.
+ *
+ * One serving iteration of the Echo paper (arXiv 2504.03651) over a paged KV
+ * cache: the new keys/values of every scheduled token are appended into
+ * fixed-size cache blocks, then the new tokens of chunked-prefill rows and
+ * decode rows attend causally to their row's cached and new tokens through
+ * per-row block tables, where rows of a prefix group alias the same blocks
+ * (Section 2.1 "Prefill and decode" and "Chunked prefills"; Section 4.2, KV
+ * cache divided into fixed-size blocks; Section 6, prefix reuse by automatic
+ * prefix caching).  Block copy duplicates whole blocks (copy-on-write).
+ *
+ * Conventions shared by every entry point
+ *   - Pointers named h_* are host memory; every other pointer is device
+ *     memory on the current HIP device.  All buffers belong to the caller and
+ *     must outlive the work enqueued on `stream` (a hipStream_t, NULL for the
+ *     default stream).  Calls return after enqueueing; they do not
+ *     synchronise.
+ *   - Validation happens before anything is enqueued: a call that returns an
+ *     error has enqueued nothing and changed nothing.
+ *   - Return values are echo_status_t codes (0 on success, negative on error);
+ *     echo_status_string() names a code and echo_last_error() gives the
+ *     calling thread's most recent error detail.
+ *   - Nothing throws across the ABI.  Calls from several host threads are
+ *     safe; work enqueued on the same stream runs in call order.
+ *
+ * Pool layout (block_size 16; head_dim 64 or 128):
+ *   K codes  [num_blocks][num_kv_heads][16][head_dim]
+ *   V codes  [num_blocks][num_kv_heads][head_dim][16]   (block-transposed)
+ *   bf16 pools store bf16; e4m3 pools store OCP e4m3fn bytes plus fp32 scales
+ *   k_scale / v_scale [num_blocks][num_kv_heads]: the value of a code is
+ *   e4m3(code) * scale of its (block, head).
+ * Token-major tensors: q [T][Hq][head_dim] bf16, k_new / v_new
+ *   [T][Hkv][head_dim] bf16, out [T][Hq][head_dim] fp32, where token t of row
+ *   r is q_start[r] + i for its i-th new token, at position
+ *   seq_lens[r] - (q_start[r+1] - q_start[r]) + i of the row.
+ */
+#ifndef ECHO_H
+#define ECHO_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    ECHO_OK = 0,
+    ECHO_E_INVALID = -1,      /* malformed argument or metadata */
+    ECHO_E_RANGE = -2,        /* a block id outside [0, num_blocks) */
+    ECHO_E_ALIAS_WRITE = -3,  /* an append would write a block another row also reads */
+    ECHO_E_WORKSPACE = -4,    /* workspace missing or smaller than required */
+    ECHO_E_UNSUPPORTED = -5,  /* head_dim, block_size or dtype not supported */
+    ECHO_E_HIP = -6           /* the HIP runtime reported an error */
+} echo_status_t;
+
+typedef enum { ECHO_KV_BF16 = 0, ECHO_KV_FP8_E4M3 = 1 } echo_kv_dtype_t;
+typedef enum { ECHO_ROW_DECODE = 0, ECHO_ROW_PREFILL = 1 } echo_row_kind_t;
+
+/* The paged KV cache of one layer (Section 4.2: fixed-size blocks allocated
+ * non-contiguously).  Device memory owned by the caller. */
+typedef struct {
+    void *k;                  /* K codes, layout above */
+    void *v;                  /* V codes, layout above */
+    float *k_scale;           /* e4m3 only: [num_blocks][num_kv_heads]; else NULL */
+    float *v_scale;
+    int32_t num_blocks;
+    int32_t num_kv_heads;
+    int32_t head_dim;         /* 64 or 128 */
+    int32_t block_size;       /* must be 16 */
+    int32_t dtype;            /* echo_kv_dtype_t */
+} echo_kv_pool_t;
+
+/* The rows of one iteration (Section 2.1: decode batching and chunked
+ * prefill in one batch).  Device arrays, plus optional host mirrors with the
+ * same contents.  The mirrors enable full validation (block ranges, aliased
+ * writes) and are required by echo_attn_mixed, whose work plan (prefix
+ * groups, key splits) is built on the host. */
+typedef struct {
+    int32_t num_rows;             /* B */
+    int32_t max_blocks_per_row;   /* row stride of block_tables */
+    int32_t num_tokens;           /* T = q_start[B] */
+    int32_t max_q_len;            /* >= every row's new-token count */
+    int32_t max_seq_len;          /* >= every seq_lens[r] */
+    const int32_t *block_tables;  /* [B][max_blocks_per_row]; entry j holds positions
+                                     16j..16j+15; entries at or past ceil(L/16) unused */
+    const int32_t *seq_lens;      /* [B] L_r: cached tokens + this call's new tokens */
+    const int32_t *q_start;       /* [B+1] prefix sums of new-token counts, q_start[0]=0 */
+    const uint8_t *row_kind;      /* [B] echo_row_kind_t; decode rows add exactly one token */
+    const int32_t *h_block_tables;  /* optional host mirrors (all four or none) */
+    const int32_t *h_seq_lens;
+    const int32_t *h_q_start;
+    const uint8_t *h_row_kind;
+} echo_batch_t;
+
+/* Append (Section 2.1: decode appends the new token's KV state to the cache;
+ * prefill generates and caches it).  For token i of row r at position p,
+ * writes k_new[t] / v_new[t] (bf16 [T][Hkv][head_dim]) into slot p % 16 of
+ * block block_tables[r][p / 16].  e4m3 pools: a block whose slot 0 is written
+ * by this call gets, per KV head, scale fp32(amax / 448) over the values this
+ * call writes into it (1 when amax is 0); other blocks keep their scale; each
+ * code is the round-to-nearest-even, saturating e4m3 encoding of the
+ * correctly rounded fp32 quotient value / scale.  Every block written must be
+ * referenced by exactly one row (copy-on-write first with echo_block_copy);
+ * with host mirrors a violation returns ECHO_E_ALIAS_WRITE.  Without mirrors
+ * only scalar checks run and the caller guarantees the metadata. */
+int echo_kv_append(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *k_new,
+                   const void *v_new, void *stream);
+
+/* Mixed attention (Section 2.1: prefill chunks and decode rows batched in
+ * one iteration; Section 6: rows of a prefix group reuse the same cached
+ * blocks).  For every new token t of row r at position p and query head h,
+ *   out[t][h] = sum_{j<=p} softmax_j(sm_scale * q[t][h] . K_r[j][g]) V_r[j][g],
+ * with g = h / (num_q_heads / num_kv_heads) and K_r/V_r the row's logical
+ * sequence read through its block table.  Run echo_kv_append for the same
+ * iteration first: attention reads the new tokens from the pool.  Blocks
+ * that several decode rows share are read once per KV head for all of them.
+ * q: bf16 [T][num_q_heads][head_dim]; out: fp32 [T][num_q_heads][head_dim].
+ * workspace: device scratch of at least echo_attn_workspace_bytes() bytes,
+ * 256-byte aligned, not used concurrently by another call.  Host mirrors
+ * are required (ECHO_E_INVALID without them). */
+int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
+                    int32_t num_q_heads, float sm_scale, float *out, void *workspace,
+                    size_t workspace_bytes, void *stream);
+
+/* Workspace bytes echo_attn_mixed needs for this batch (from the host
+ * mirrors), or 0 if the arguments are invalid. */
+size_t echo_attn_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                                 int32_t num_q_heads);
+
+/* Block copy (copy-on-write of blocks that prefix-sharing rows alias; the
+ * paper's automatic prefix caching, Section 6, implies it).  For each pair
+ * (src, dst) of pairs (device int32 [n][2]) copies K, V and, for e4m3 pools,
+ * both scales of block src into block dst, byte for byte.  Requires src !=
+ * dst, distinct dst, and no dst that is also a src (ECHO_E_INVALID, checked
+ * when the host mirror h_pairs is given; ids are range-checked then too, and
+ * on the device always, where out-of-range pairs are skipped). */
+int echo_block_copy(const echo_kv_pool_t *pool, const int32_t *pairs, int32_t n_pairs,
+                    const int32_t *h_pairs, void *stream);
+
+/* What the planner made of a batch: a host-only call (no GPU work). */
+typedef struct {
+    int64_t work_items;         /* wave-sized attention work items */
+    int64_t decode_items;
+    int64_t prefill_items;
+    int64_t shared_segments;    /* block runs read once for several decode rows */
+    int64_t partial_slots;      /* split results merged after the main pass */
+    int64_t merged_queries;     /* (token, head) pairs that need the merge */
+    int64_t unique_kv_tokens;   /* per KV head: distinct (block, slot) pairs read */
+    int64_t logical_kv_tokens;  /* per KV head: sum over rows of seq_lens */
+    int64_t causal_pairs;       /* per query head: sum over queries of visible keys */
+    int64_t workspace_bytes;
+} echo_plan_stats_t;
+
+/* Validates the batch (host mirrors required) and fills *stats. */
+int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                         int32_t num_q_heads, echo_plan_stats_t *stats);
+
+/* Host-only validation of pool and batch as echo_kv_append (for_append = 1)
+ * or echo_attn_mixed (for_append = 0) would do it; no GPU work. */
+int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t for_append);
+
+/* Static name of a status code. */
+const char *echo_status_string(int status);
+
+/* The calling thread's most recent error detail ("" when none). */
+const char *echo_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* ECHO_H */

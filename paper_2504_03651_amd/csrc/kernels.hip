@@ -1,0 +1,445 @@
+// kernels.hip -- gfx950 kernels of the mixed paged-attention iteration.
+//
+//   append_kernel       scatter new K/V into the paged pool (bf16 bit copy,
+//                       or e4m3 quantisation with per-(block, head) scales)
+//   block_copy_kernel   whole-block copy-on-write
+//   attn_items_kernel   one wave per work item: up to 16 query vectors against
+//                       a run of 16-token blocks, online softmax, bf16 MFMA
+//   merge_kernel        log-sum-exp merge of split / segment partial results
+//
+// MFMA tile orientation (v_mfma_f32_16x16x32_bf16, wave64):
+//   S^T[key][query] = K[key][d] * Q^T[d][query]     (keys on rows)
+//   O^T[d][query]  += V^T[d][key] * P^T[key][query]
+// so each lane ends up owning one query column and the softmax statistics of
+// that query never leave the lane's 16-lane column group.  K blocks are stored
+// [16][D] and V blocks [D][16], which makes every MFMA operand one contiguous
+// 16-byte (bf16) or 8-byte (e4m3) load straight from the pool.
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "kernels.hpp"
+
+namespace echo {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+
+// ------------------------------------------------------------------- codecs
+
+// OCP e4m3fn byte -> exact bf16 bits (every e4m3 value is a bf16 value).
+__device__ __forceinline__ uint32_t e4m3_to_bf16_bits(uint32_t x) {
+    const uint32_t s = (x & 0x80u) << 8;
+    const uint32_t e = (x >> 3) & 15u, m = x & 7u;
+    if (e == 15u && m == 7u) return s | 0x7FC0u;
+    if (e != 0u) return s | ((e + 120u) << 7) | (m << 4);
+    // subnormal m * 2^-9: exact through fp32
+    const float f = (float)m * 0x1p-9f;
+    return s | (__float_as_uint(f) >> 16);
+}
+
+__device__ __forceinline__ bf16x8_t e4m3x8_to_bf16x8(u32x2_t w) {
+    u32x4_t o;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+        const uint32_t word = w[k >> 1] >> (16 * (k & 1));
+        o[k] = e4m3_to_bf16_bits(word & 0xFFu) | (e4m3_to_bf16_bits((word >> 8) & 0xFFu) << 16);
+    }
+    return __builtin_bit_cast(bf16x8_t, o);
+}
+
+// fp32 -> OCP e4m3fn, round to nearest even, saturating to +-448.
+__device__ __forceinline__ uint32_t f32_to_e4m3(float y) {
+    const uint32_t u = __float_as_uint(y);
+    const uint32_t sign = (u >> 24) & 0x80u;
+    const uint32_t a = u & 0x7FFFFFFFu;
+    if (a > 0x7F800000u) return 0x7Fu;               // NaN
+    if (a >= 0x43E00000u) return sign | 0x7Eu;       // |y| >= 448 (and inf)
+    if (a < 0x3C800000u) {                           // |y| < 2^-6: step 2^-9
+        const float q = __builtin_rintf(__uint_as_float(a) * 512.0f);
+        return sign | (uint32_t)q;                   // q == 8 encodes 2^-6
+    }
+    int32_t e = (int32_t)(a >> 23) - 127;            // -6 .. 8
+    uint32_t mant = a & 0x7FFFFFu;
+    uint32_t r = mant >> 20, rem = mant & 0xFFFFFu;
+    if (rem > 0x80000u || (rem == 0x80000u && (r & 1u))) ++r;
+    if (r == 8u) { r = 0; ++e; }
+    const uint32_t code = ((uint32_t)(e + 7) << 3) | r;
+    return sign | (code > 0x7Eu ? 0x7Eu : code);
+}
+
+__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// ------------------------------------------------------------------- append
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t unit = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (unit >= a.n_units) return;
+    const int h = (int)(unit % a.num_kv_heads);
+    const int64_t rest = unit / a.num_kv_heads;
+    const int k = (int)(rest % a.blocks_per_row);
+    const int r = (int)(rest / a.blocks_per_row);
+    const int t0 = a.q_start[r];
+    const int q = a.q_start[r + 1] - t0;
+    const int L = a.seq_lens[r];
+    const int p0 = L - q;
+    if (q <= 0 || p0 < 0) return;
+    const int j = p0 / 16 + k;
+    if (j > (L - 1) / 16 || j >= a.max_blocks_per_row) return;
+    const int blk = a.block_tables[(int64_t)r * a.max_blocks_per_row + j];
+    if (blk < 0 || blk >= a.num_blocks) return;
+    const int lo = p0 > 16 * j ? p0 : 16 * j;
+    const int hi = L < 16 * j + 16 ? L : 16 * j + 16;
+    const int64_t tile = ((int64_t)blk * a.num_kv_heads + h) * 16 * D;
+    const uint16_t *ksrc = a.k_new + ((int64_t)(t0 + lo - p0) * a.num_kv_heads + h) * D;
+    const uint16_t *vsrc = a.v_new + ((int64_t)(t0 + lo - p0) * a.num_kv_heads + h) * D;
+    const int64_t tok_stride = (int64_t)a.num_kv_heads * D;
+    const int n = hi - lo;
+
+    if constexpr (!FP8) {
+        uint16_t *kdst = (uint16_t *)a.k + tile;
+        uint16_t *vdst = (uint16_t *)a.v + tile;
+        constexpr int LPT = D / 8;      // lanes per token row (16 bytes each)
+        constexpr int TPP = 64 / LPT;   // token rows per pass
+        for (int i = lane / LPT; i < n; i += TPP) {
+            const u32x4_t w = *(const u32x4_t *)(ksrc + i * tok_stride + (lane % LPT) * 8);
+            *(u32x4_t *)(kdst + ((lo + i) & 15) * D + (lane % LPT) * 8) = w;
+        }
+        for (int d = lane; d < D; d += 64)
+            for (int i = 0; i < n; ++i)
+                vdst[d * 16 + ((lo + i) & 15)] = vsrc[i * tok_stride + d];
+    } else {
+        uint8_t *kdst = (uint8_t *)a.k + tile;
+        uint8_t *vdst = (uint8_t *)a.v + tile;
+        const int64_t si = (int64_t)blk * a.num_kv_heads + h;
+        float sk, sv;
+        if (16 * j >= p0) {  // slot 0 written by this call: fresh scales
+            float ak = 0.f, av = 0.f;
+            for (int d = lane; d < D; d += 64)
+                for (int i = 0; i < n; ++i) {
+                    ak = fmaxf(ak, fabsf(bf16_bits_to_f32(ksrc[i * tok_stride + d])));
+                    av = fmaxf(av, fabsf(bf16_bits_to_f32(vsrc[i * tok_stride + d])));
+                }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                ak = fmaxf(ak, __shfl_xor(ak, off));
+                av = fmaxf(av, __shfl_xor(av, off));
+            }
+            sk = ak == 0.f ? 1.f : ak / 448.0f;
+            sv = av == 0.f ? 1.f : av / 448.0f;
+            if (lane == 0) {
+                a.k_scale[si] = sk;
+                a.v_scale[si] = sv;
+            }
+        } else {
+            sk = a.k_scale[si];
+            sv = a.v_scale[si];
+        }
+        for (int d = lane; d < D; d += 64)
+            for (int i = 0; i < n; ++i) {
+                const int slot = (lo + i) & 15;
+                kdst[slot * D + d] =
+                    (uint8_t)f32_to_e4m3(bf16_bits_to_f32(ksrc[i * tok_stride + d]) / sk);
+                vdst[d * 16 + slot] =
+                    (uint8_t)f32_to_e4m3(bf16_bits_to_f32(vsrc[i * tok_stride + d]) / sv);
+            }
+    }
+}
+
+// --------------------------------------------------------------- block copy
+
+__global__ __launch_bounds__(256) void block_copy_kernel(BlockCopyArgs a) {
+    const int64_t unit = blockIdx.x;
+    const int pair = (int)(unit / a.chunks);
+    const int chunk = (int)(unit % a.chunks);
+    if (pair >= a.n_pairs) return;
+    const int src = a.pairs[2 * pair], dst = a.pairs[2 * pair + 1];
+    if (src < 0 || src >= a.num_blocks || dst < 0 || dst >= a.num_blocks) return;
+    const int64_t words = a.block_bytes / 16;
+    const u32x4_t *ks = (const u32x4_t *)((const uint8_t *)a.k + (int64_t)src * a.block_bytes);
+    const u32x4_t *vs = (const u32x4_t *)((const uint8_t *)a.v + (int64_t)src * a.block_bytes);
+    u32x4_t *kd = (u32x4_t *)((uint8_t *)a.k + (int64_t)dst * a.block_bytes);
+    u32x4_t *vd = (u32x4_t *)((uint8_t *)a.v + (int64_t)dst * a.block_bytes);
+    const int64_t base = (int64_t)chunk * 1024;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+        const int64_t w = base + e * 256 + threadIdx.x;
+        if (w < words) {
+            kd[w] = ks[w];
+            vd[w] = vs[w];
+        }
+    }
+    if (a.k_scale && chunk == 0) {
+        for (int h = threadIdx.x; h < a.num_kv_heads; h += 256) {
+            a.k_scale[(int64_t)dst * a.num_kv_heads + h] = a.k_scale[(int64_t)src * a.num_kv_heads + h];
+            a.v_scale[(int64_t)dst * a.num_kv_heads + h] = a.v_scale[(int64_t)src * a.num_kv_heads + h];
+        }
+    }
+}
+
+// ---------------------------------------------------------------- attention
+
+template <bool FP8>
+struct KV;
+template <>
+struct KV<false> {
+    typedef uint16_t T;
+    typedef u32x4_t Raw;   // 8 bf16
+    static __device__ __forceinline__ Raw load(const T *p) { return *(const Raw *)p; }
+    static __device__ __forceinline__ bf16x8_t widen(Raw r) { return __builtin_bit_cast(bf16x8_t, r); }
+    // zero element e (0..7) where bit e of keep is clear
+    static __device__ __forceinline__ Raw mask(Raw r, uint32_t keep) {
+#pragma unroll
+        for (int w = 0; w < 4; ++w) {
+            const uint32_t m = ((keep >> (2 * w)) & 1u ? 0x0000FFFFu : 0u) |
+                               ((keep >> (2 * w + 1)) & 1u ? 0xFFFF0000u : 0u);
+            r[w] &= m;
+        }
+        return r;
+    }
+};
+template <>
+struct KV<true> {
+    typedef uint8_t T;
+    typedef u32x2_t Raw;   // 8 e4m3
+    static __device__ __forceinline__ Raw load(const T *p) { return *(const Raw *)p; }
+    static __device__ __forceinline__ bf16x8_t widen(Raw r) { return e4m3x8_to_bf16x8(r); }
+    static __device__ __forceinline__ Raw mask(Raw r, uint32_t keep) {
+#pragma unroll
+        for (int w = 0; w < 2; ++w) {
+            uint32_t m = 0;
+#pragma unroll
+            for (int b = 0; b < 4; ++b) m |= ((keep >> (4 * w + b)) & 1u) ? (0xFFu << (8 * b)) : 0u;
+            r[w] &= m;
+        }
+        return r;
+    }
+};
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
+    typedef KV<FP8> kv;
+    typedef typename kv::T KT;
+    typedef typename kv::Raw Raw;
+    constexpr int NC = D / 32;  // 32-wide d chunks of the QK contraction
+    constexpr int NT = D / 16;  // 16-row d tiles of O^T
+
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int idx = blockIdx.x * 4 + wave;
+    if (idx >= a.n_items) return;
+    const int32_t *ip = (const int32_t *)(a.items + idx);
+    const int tok_off = __builtin_amdgcn_readfirstlane(ip[0]);
+    const int shape = __builtin_amdgcn_readfirstlane(ip[1]);
+    const int h0 = __builtin_amdgcn_readfirstlane(ip[2]);
+    const int kvh = __builtin_amdgcn_readfirstlane(ip[3]);
+    const int bt_row = __builtin_amdgcn_readfirstlane(ip[4]);
+    const int key_begin = __builtin_amdgcn_readfirstlane(ip[5]);
+    const int key_end = __builtin_amdgcn_readfirstlane(ip[6]);
+    const int part = __builtin_amdgcn_readfirstlane(ip[7]);
+
+    const int g4 = lane >> 4;   // 16-lane group: selects 8 of each 32 k-values
+    const int c16 = lane & 15;  // MFMA row (A) / column (B, C) index
+    const int nt = shape & 0xFF, nh = (shape >> 8) & 0xFF;
+    const int qi = c16 / nh, qj = c16 - (c16 / nh) * nh;
+    const bool qvalid = qi < nt;
+    int tok = 0, klim = 0;
+    if (qvalid) {
+        tok = (shape & kItemConsecutive) ? tok_off + qi : a.tok_list[tok_off + qi];
+        klim = a.klim[tok];
+    }
+    const int head = h0 + qj;
+
+    // Q^T as the B operand: column c16, k-values d = 32c + 8*g4 .. +8
+    bf16x8_t qf[NC];
+    {
+        const uint16_t *qp = a.q + ((int64_t)tok * a.num_q_heads + head) * D + 8 * g4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            u32x4_t w = {0u, 0u, 0u, 0u};
+            if (qvalid) w = *(const u32x4_t *)(qp + 32 * c);
+            qf[c] = __builtin_bit_cast(bf16x8_t, w);
+        }
+    }
+
+    f32x4_t acc[NT];
+#pragma unroll
+    for (int i = 0; i < NT; ++i) acc[i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    float m_run = -INFINITY, l_run = 0.f;
+
+    const int32_t *btr = a.block_tables + (int64_t)bt_row * a.max_blocks_per_row;
+    const int64_t blk_stride = (int64_t)a.num_kv_heads * 16 * D;
+    const KT *kbase = (const KT *)a.k + (int64_t)kvh * 16 * D;
+    const KT *vbase = (const KT *)a.v + (int64_t)kvh * 16 * D;
+    // S^T tile t, row c16 holds key 8*(c16>>2) + 4t + (c16&3) of the 32-key
+    // window, so lane (g4, c16) receives keys 8*g4 .. 8*g4+7 of its column.
+    const int ksel = c16 >= 8;
+    const int kslot = 8 * ((c16 >> 2) & 1) + (c16 & 3);
+    // V^T tile i, row c16 is d = 16i + c16; k-values are keys 8*g4 .. +8
+    const int vsel = g4 >= 2;
+    const int vslot = 8 * (g4 & 1);
+    const float scale = a.scale_log2;
+
+    for (int kb = key_begin; kb < key_end; kb += 32) {
+        const int jb = kb >> 4;
+        const int b0 = btr[jb];
+        const bool has1 = kb + 16 < key_end;
+        const int b1 = has1 ? btr[jb + 1] : b0;
+        const int kblk = ksel ? b1 : b0;
+        const int vblk = vsel ? b1 : b0;
+
+        Raw kr[2][NC], vr[NT];
+        const KT *kp = kbase + (int64_t)kblk * blk_stride + kslot * D + 8 * g4;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int c = 0; c < NC; ++c) kr[t][c] = kv::load(kp + 4 * t * D + 32 * c);
+        const KT *vp = vbase + (int64_t)vblk * blk_stride + c16 * 16 + vslot;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) vr[i] = kv::load(vp + i * 256);
+
+        f32x4_t s[2];
+#pragma unroll
+        for (int t = 0; t < 2; ++t) {
+            s[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int c = 0; c < NC; ++c)
+                s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(kr[t][c]), qf[c], s[t],
+                                                               0, 0, 0);
+        }
+
+        float sk = scale, sv = 1.f;
+        if constexpr (FP8) {
+            sk = scale * a.k_scale[(int64_t)vblk * a.num_kv_heads + kvh];
+            sv = a.v_scale[(int64_t)vblk * a.num_kv_heads + kvh];
+        }
+        const int key0 = kb + 8 * g4;
+        float p[8];
+        float mx = -INFINITY;
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+            for (int r = 0; r < 4; ++r) {
+                const int key = key0 + 4 * t + r;
+                const float v = s[t][r] * sk;
+                p[4 * t + r] = (key < key_end && key < klim) ? v : -INFINITY;
+                mx = fmaxf(mx, p[4 * t + r]);
+            }
+        mx = fmaxf(mx, __shfl_xor(mx, 16));
+        mx = fmaxf(mx, __shfl_xor(mx, 32));
+        const float m_new = fmaxf(m_run, mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(m_run - m_use);
+        float psum = 0.f;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) {
+            p[e] = exp2f(p[e] - m_use);
+            psum += p[e];
+        }
+        l_run = l_run * alpha + psum;
+        m_run = m_new;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) acc[i] *= alpha;
+
+        bf16x8_t pf;
+#pragma unroll
+        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)(p[e] * sv);
+
+        if (kb + 32 > key_end) {  // zero V columns past the end: 0 * NaN is NaN
+            const int valid = key_end - key0;
+            const uint32_t keep = valid >= 8 ? 0xFFu : (valid <= 0 ? 0u : ((1u << valid) - 1u));
+#pragma unroll
+            for (int i = 0; i < NT; ++i) vr[i] = kv::mask(vr[i], keep);
+        }
+#pragma unroll
+        for (int i = 0; i < NT; ++i)
+            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(vr[i]), pf, acc[i], 0, 0, 0);
+    }
+
+    float l_tot = l_run + __shfl_xor(l_run, 16);
+    l_tot += __shfl_xor(l_tot, 32);
+    if (!qvalid) return;
+    const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+    float *dst;
+    if (part < 0) {
+        dst = a.out + ((int64_t)tok * a.num_q_heads + head) * D;
+    } else {
+        dst = a.part_o + (int64_t)(part + c16) * D;
+        if (g4 == 0) a.part_lse[part + c16] = l_tot > 0.f ? m_run + log2f(l_tot) : -INFINITY;
+    }
+#pragma unroll
+    for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i + 4 * g4) = acc[i] * inv;
+}
+
+// -------------------------------------------------------------------- merge
+
+template <int D>
+__global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= a.n_merge) return;
+    const int q = a.merge_q[m];
+    const int s0 = a.merge_ptr[m], s1 = a.merge_ptr[m + 1];
+    float mx = -INFINITY;
+    for (int s = s0; s < s1; ++s) mx = fmaxf(mx, a.part_lse[a.merge_slot[s]]);
+    constexpr int PER = D / 64;
+    float acc[PER];
+#pragma unroll
+    for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+    float wsum = 0.f;
+    for (int s = s0; s < s1; ++s) {
+        const int slot = a.merge_slot[s];
+        const float lse = a.part_lse[slot];
+        const float w = lse == -INFINITY ? 0.f : exp2f(lse - mx);
+        wsum += w;
+#pragma unroll
+        for (int e = 0; e < PER; ++e) acc[e] += w * a.part_o[(int64_t)slot * D + lane * PER + e];
+    }
+    const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+#pragma unroll
+    for (int e = 0; e < PER; ++e) a.out[(int64_t)q * D + lane * PER + e] = acc[e] * inv;
+}
+
+// ------------------------------------------------------------------ launchers
+
+hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s) {
+    if (a.n_units == 0) return hipSuccess;
+    const dim3 grid((unsigned)((a.n_units + 3) / 4)), block(256);
+    if (head_dim == 64 && !fp8) hipLaunchKernelGGL((append_kernel<64, false>), grid, block, 0, s, a);
+    else if (head_dim == 64) hipLaunchKernelGGL((append_kernel<64, true>), grid, block, 0, s, a);
+    else if (!fp8) hipLaunchKernelGGL((append_kernel<128, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((append_kernel<128, true>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s) {
+    if (a.n_pairs == 0) return hipSuccess;
+    const dim3 grid((unsigned)((int64_t)a.n_pairs * a.chunks)), block(256);
+    hipLaunchKernelGGL(block_copy_kernel, grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, int head_dim, bool fp8,
+                            hipStream_t s) {
+    if (a.n_items > 0) {
+        const dim3 grid((unsigned)((a.n_items + 3) / 4)), block(256);
+        if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_items_kernel<64, false>), grid, block, 0, s, a);
+        else if (head_dim == 64) hipLaunchKernelGGL((attn_items_kernel<64, true>), grid, block, 0, s, a);
+        else if (!fp8) hipLaunchKernelGGL((attn_items_kernel<128, false>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((attn_items_kernel<128, true>), grid, block, 0, s, a);
+        hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+    }
+    if (m.n_merge > 0) {
+        const dim3 grid((unsigned)((m.n_merge + 3) / 4)), block(256);
+        if (head_dim == 64) hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, s, m);
+        else hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, s, m);
+        return hipGetLastError();
+    }
+    return hipSuccess;
+}
+
+}  // namespace echo

@@ -1,0 +1,55 @@
+// kernels.hpp -- argument blocks and launchers of the gfx950 kernels.
+#pragma once
+#include <hip/hip_runtime_api.h>
+#include <stdint.h>
+
+#include "plan.hpp"
+
+namespace echo {
+
+struct AppendArgs {
+    void *k, *v;
+    float *k_scale, *v_scale;
+    const uint16_t *k_new, *v_new;  // [T][Hkv][D] bf16 bits
+    const int32_t *block_tables, *seq_lens, *q_start;
+    int32_t num_blocks, num_kv_heads, max_blocks_per_row;
+    int32_t blocks_per_row;         // written blocks per row, upper bound
+    int64_t n_units;                // rows * blocks_per_row * num_kv_heads
+};
+
+struct BlockCopyArgs {
+    void *k, *v;
+    float *k_scale, *v_scale;       // NULL unless e4m3
+    const int32_t *pairs;
+    int32_t n_pairs, num_blocks, num_kv_heads;
+    int64_t block_bytes;            // bytes of one block of K (same for V)
+    int32_t chunks;                 // 16 KiB chunks per block
+};
+
+struct AttnArgs {
+    const AttnItem *items;
+    int32_t n_items;
+    const int32_t *tok_list, *klim;
+    const uint16_t *q;              // [T][Hq][D] bf16 bits
+    int32_t num_q_heads, num_kv_heads;
+    const void *k, *v;
+    const float *k_scale, *v_scale;
+    const int32_t *block_tables;
+    int32_t max_blocks_per_row;
+    float scale_log2;               // sm_scale * log2(e)
+    float *out, *part_o, *part_lse;
+};
+
+struct MergeArgs {
+    int32_t n_merge;
+    const int32_t *merge_q, *merge_ptr, *merge_slot;
+    const float *part_o, *part_lse;
+    float *out;
+};
+
+hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
+hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, int head_dim, bool fp8,
+                            hipStream_t s);
+
+}  // namespace echo

@@ -1,0 +1,90 @@
+// plan.hpp -- work plan of one mixed attention call, built on the host from
+// the batch's host mirrors and uploaded into the caller's workspace.
+//
+// A work item is what one 64-lane wave computes: up to 16 query vectors
+// (tokens x query heads of one KV head) against one contiguous key range of
+// one row's block table.  Decode rows whose leading blocks are the same
+// physical blocks (a prefix group, Section 6 of the paper: prefix reuse via
+// automatic prefix caching) are found with a trie over their block ids; each
+// shared run of blocks becomes one segment whose keys are read once for the
+// query vectors of every row in it.  Long key ranges are cut into splits;
+// split and segment results are partial softmax states merged afterwards.
+#pragma once
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+namespace echo {
+
+constexpr int kBlock = 16;
+constexpr int kWaveQueries = 16;   // query vectors per wave (MFMA N dimension)
+constexpr int kWavesPerGroup = 4;  // waves per workgroup
+
+// flags in AttnItem::shape
+constexpr int32_t kItemConsecutive = 1 << 16;  // tokens tok_off, tok_off+1, ...
+
+struct AttnItem {      // 32 bytes
+    int32_t tok_off;   // first token, or offset into the plan's token list
+    int32_t shape;     // nt | nh << 8 | flags
+    int32_t h0;        // first query head
+    int32_t kvh;       // KV head
+    int32_t bt_row;    // row whose block table supplies the block ids
+    int32_t key_begin; // first key position, a multiple of 16
+    int32_t key_end;   // one past the last key position
+    int32_t part;      // first partial slot, or -1: write `out` directly
+};
+static_assert(sizeof(AttnItem) == 32, "item layout");
+
+// Offsets (in 4-byte words from the start of the workspace) of each region.
+struct PlanLayout {
+    int64_t n_items = 0;
+    int64_t n_tok_list = 0;
+    int64_t n_tokens = 0;
+    int64_t n_merge = 0;
+    int64_t n_merge_slots = 0;
+    int64_t n_slots = 0;
+    int32_t head_dim = 0;
+    int64_t off_items = 0;      // AttnItem[n_items]
+    int64_t off_tok_list = 0;   // int32[n_tok_list]
+    int64_t off_klim = 0;       // int32[n_tokens]: keys visible to each token
+    int64_t off_merge_q = 0;    // int32[n_merge]: t * Hq + h
+    int64_t off_merge_ptr = 0;  // int32[n_merge + 1]
+    int64_t off_merge_slot = 0; // int32[n_merge_slots]
+    int64_t upload_words = 0;   // everything above is uploaded
+    int64_t off_part_lse = 0;   // float[n_slots]
+    int64_t off_part_o = 0;     // float[n_slots][head_dim]
+    int64_t total_words = 0;
+};
+
+struct PlanStats {
+    int64_t decode_items = 0, prefill_items = 0, shared_segments = 0;
+    int64_t unique_kv_tokens = 0, logical_kv_tokens = 0, causal_pairs = 0;
+};
+
+struct HostBatch {
+    int32_t num_rows, mbr, num_tokens, max_q_len, max_seq_len;
+    const int32_t *bt, *seq_lens, *q_start;
+    const uint8_t *kind;
+};
+
+struct PlanOptions {
+    int split_blocks = 32;  // key blocks per decode split
+};
+
+// Host plan under construction (reused between calls on the same thread).
+struct Plan {
+    std::vector<AttnItem> items;
+    std::vector<int32_t> tok_list, klim, merge_q, merge_ptr, merge_slot;
+    PlanLayout layout;
+    PlanStats stats;
+};
+
+// Builds the plan for a validated batch.  Returns 0 or an echo_status_t.
+int build_plan(const HostBatch &b, int32_t num_kv_heads, int32_t num_q_heads,
+               int32_t head_dim, const PlanOptions &opt, Plan &plan);
+
+// Serialises the uploaded regions of `plan` into `dst` (layout.upload_words
+// words).
+void pack_plan(const Plan &plan, void *dst);
+
+}  // namespace echo

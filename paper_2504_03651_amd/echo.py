@@ -1,0 +1,245 @@
+"""Python binding of libecho.so (include/echo.h): argument marshalling only.
+
+Every step of the iteration runs in the HIP library; this module allocates
+device buffers with PyTorch, fills the C structs and calls the entry points
+on PyTorch's current stream.  If the library has not been built, every call
+raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libecho.so")
+
+ECHO_OK = 0
+ECHO_E_INVALID = -1
+ECHO_E_RANGE = -2
+ECHO_E_ALIAS_WRITE = -3
+ECHO_E_WORKSPACE = -4
+ECHO_E_UNSUPPORTED = -5
+ECHO_E_HIP = -6
+KV_BF16 = 0
+KV_FP8_E4M3 = 1
+
+SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes", "echo_block_copy",
+           "echo_attn_plan_stats", "echo_validate", "echo_status_string", "echo_last_error"]
+
+
+class EchoError(RuntimeError):
+    def __init__(self, code: int, where: str, detail: str):
+        super().__init__(f"{where}: {status_string(code)} ({code}): {detail}")
+        self.code = code
+
+
+class CPool(ctypes.Structure):
+    _fields_ = [("k", ctypes.c_void_p), ("v", ctypes.c_void_p),
+                ("k_scale", ctypes.c_void_p), ("v_scale", ctypes.c_void_p),
+                ("num_blocks", ctypes.c_int32), ("num_kv_heads", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("block_size", ctypes.c_int32),
+                ("dtype", ctypes.c_int32)]
+
+
+class CBatch(ctypes.Structure):
+    _fields_ = [("num_rows", ctypes.c_int32), ("max_blocks_per_row", ctypes.c_int32),
+                ("num_tokens", ctypes.c_int32), ("max_q_len", ctypes.c_int32),
+                ("max_seq_len", ctypes.c_int32),
+                ("block_tables", ctypes.c_void_p), ("seq_lens", ctypes.c_void_p),
+                ("q_start", ctypes.c_void_p), ("row_kind", ctypes.c_void_p),
+                ("h_block_tables", ctypes.c_void_p), ("h_seq_lens", ctypes.c_void_p),
+                ("h_q_start", ctypes.c_void_p), ("h_row_kind", ctypes.c_void_p)]
+
+
+class CPlanStats(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "work_items", "decode_items", "prefill_items", "shared_segments", "partial_slots",
+        "merged_queries", "unique_kv_tokens", "logical_kv_tokens", "causal_pairs",
+        "workspace_bytes")]
+
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -c 'import __graft_entry__ as g; g.build()'`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, B, vp = ctypes.POINTER(CPool), ctypes.POINTER(CBatch), ctypes.c_void_p
+        L.echo_kv_append.argtypes = [P, B, vp, vp, vp]
+        L.echo_attn_mixed.argtypes = [P, B, vp, ctypes.c_int32, ctypes.c_float, vp, vp,
+                                      ctypes.c_size_t, vp]
+        L.echo_attn_workspace_bytes.argtypes = [P, B, ctypes.c_int32]
+        L.echo_attn_workspace_bytes.restype = ctypes.c_size_t
+        L.echo_block_copy.argtypes = [P, vp, ctypes.c_int32, vp, vp]
+        L.echo_attn_plan_stats.argtypes = [P, B, ctypes.c_int32, ctypes.POINTER(CPlanStats)]
+        L.echo_validate.argtypes = [P, B, ctypes.c_int32]
+        L.echo_status_string.argtypes = [ctypes.c_int]
+        L.echo_status_string.restype = ctypes.c_char_p
+        L.echo_last_error.argtypes = []
+        L.echo_last_error.restype = ctypes.c_char_p
+        for name in ("echo_kv_append", "echo_attn_mixed", "echo_block_copy",
+                     "echo_attn_plan_stats", "echo_validate"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(code: int) -> str:
+    return lib().echo_status_string(int(code)).decode()
+
+
+def last_error() -> str:
+    return lib().echo_last_error().decode()
+
+
+def _check(code: int, where: str) -> None:
+    if code != ECHO_OK:
+        raise EchoError(code, where, last_error())
+
+
+def _np_ptr(a):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream):
+    import torch
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+# ---------------------------------------------------------------- device data
+
+
+class KVPool:
+    """A paged KV pool in device memory: K [NB][Hkv][16][D], V [NB][Hkv][D][16]."""
+
+    def __init__(self, num_blocks: int, num_kv_heads: int, head_dim: int, fp8: bool = False,
+                 device: str = "cuda"):
+        import torch
+        self.num_blocks, self.num_kv_heads, self.head_dim = num_blocks, num_kv_heads, head_dim
+        self.fp8 = bool(fp8)
+        et = torch.uint8 if self.fp8 else torch.int16
+        self.k = torch.empty((num_blocks, num_kv_heads, 16, head_dim), dtype=et, device=device)
+        self.v = torch.empty((num_blocks, num_kv_heads, head_dim, 16), dtype=et, device=device)
+        if self.fp8:
+            self.k_scale = torch.empty((num_blocks, num_kv_heads), dtype=torch.float32,
+                                       device=device)
+            self.v_scale = torch.empty_like(self.k_scale)
+        else:
+            self.k_scale = self.v_scale = None
+
+    def poison(self) -> "KVPool":
+        """Fill every slot with NaN codes (unwritten slots must never matter)."""
+        self.k.fill_(0x7F if self.fp8 else 0x7FC0)
+        self.v.fill_(0x7F if self.fp8 else 0x7FC0)
+        if self.fp8:
+            self.k_scale.fill_(float("nan"))
+            self.v_scale.fill_(float("nan"))
+        return self
+
+    def c(self) -> CPool:
+        return CPool(self.k.data_ptr(), self.v.data_ptr(),
+                     self.k_scale.data_ptr() if self.fp8 else None,
+                     self.v_scale.data_ptr() if self.fp8 else None,
+                     self.num_blocks, self.num_kv_heads, self.head_dim, 16,
+                     KV_FP8_E4M3 if self.fp8 else KV_BF16)
+
+
+class DeviceBatch:
+    """Row metadata on the device plus its host mirrors (kept alive here)."""
+
+    def __init__(self, batch, device: str = "cuda", mirrors: bool = True):
+        import torch
+        self.h_bt = np.ascontiguousarray(batch.block_tables, np.int32)
+        self.h_sl = np.ascontiguousarray(batch.seq_lens, np.int32)
+        self.h_qs = np.ascontiguousarray(batch.q_start, np.int32)
+        self.h_kind = np.ascontiguousarray(batch.row_kind, np.uint8)
+        self.num_rows = int(self.h_sl.shape[0])
+        self.mbr = int(self.h_bt.shape[1])
+        self.num_tokens = int(self.h_qs[-1])
+        q = np.diff(self.h_qs)
+        self.max_q_len = int(q.max()) if self.num_rows else 1
+        self.max_seq_len = int(self.h_sl.max()) if self.num_rows else 1
+        self.mirrors = mirrors
+        self.bt = torch.from_numpy(self.h_bt).to(device)
+        self.sl = torch.from_numpy(self.h_sl).to(device)
+        self.qs = torch.from_numpy(self.h_qs).to(device)
+        self.kind = torch.from_numpy(self.h_kind).to(device)
+
+    def c(self) -> CBatch:
+        m = self.mirrors
+        return CBatch(self.num_rows, self.mbr, self.num_tokens, self.max_q_len, self.max_seq_len,
+                      self.bt.data_ptr(), self.sl.data_ptr(), self.qs.data_ptr(),
+                      self.kind.data_ptr(),
+                      _np_ptr(self.h_bt) if m else None, _np_ptr(self.h_sl) if m else None,
+                      _np_ptr(self.h_qs) if m else None, _np_ptr(self.h_kind) if m else None)
+
+
+# ---------------------------------------------------------------- entry points
+
+
+def kv_append(pool: KVPool, batch: DeviceBatch, k_new, v_new, stream=None) -> None:
+    cp, cb = pool.c(), batch.c()
+    _check(lib().echo_kv_append(ctypes.byref(cp), ctypes.byref(cb), k_new.data_ptr(),
+                                v_new.data_ptr(), _stream(stream)), "echo_kv_append")
+
+
+def workspace_bytes(pool: KVPool, batch: DeviceBatch, num_q_heads: int) -> int:
+    cp, cb = pool.c(), batch.c()
+    n = lib().echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), int(num_q_heads))
+    if n == 0 and batch.num_rows:
+        raise EchoError(ECHO_E_INVALID, "echo_attn_workspace_bytes", last_error())
+    return int(n)
+
+
+def attn_mixed(pool: KVPool, batch: DeviceBatch, q, num_q_heads: int, sm_scale: float, out,
+               workspace, stream=None) -> None:
+    cp, cb = pool.c(), batch.c()
+    _check(lib().echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), q.data_ptr(),
+                                 int(num_q_heads), float(sm_scale), out.data_ptr(),
+                                 workspace.data_ptr(), workspace.numel() * workspace.element_size(),
+                                 _stream(stream)), "echo_attn_mixed")
+
+
+def block_copy(pool: KVPool, pairs, h_pairs=None, stream=None) -> None:
+    n = int(pairs.shape[0])
+    hp = None if h_pairs is None else np.ascontiguousarray(h_pairs, np.int32)
+    cp = pool.c()
+    _check(lib().echo_block_copy(ctypes.byref(cp), pairs.data_ptr() if n else None, n,
+                                 _np_ptr(hp), _stream(stream)), "echo_block_copy")
+
+
+def plan_stats(cpool: CPool, cbatch: CBatch, num_q_heads: int) -> dict:
+    st = CPlanStats()
+    _check(lib().echo_attn_plan_stats(ctypes.byref(cpool), ctypes.byref(cbatch),
+                                      int(num_q_heads), ctypes.byref(st)), "echo_attn_plan_stats")
+    return {name: int(getattr(st, name)) for name, _ in CPlanStats._fields_}
+
+
+def validate(cpool: CPool, cbatch: CBatch, for_append: bool) -> int:
+    return int(lib().echo_validate(ctypes.byref(cpool), ctypes.byref(cbatch), int(for_append)))
+
+
+def host_structs(w, fake_device_ptr: int = 0x1000):
+    """C structs of workload ``w`` for host-only calls (validation, plan
+    statistics): device pointers are placeholders that are never touched."""
+    bt = np.ascontiguousarray(w.batch.block_tables, np.int32)
+    sl = np.ascontiguousarray(w.batch.seq_lens, np.int32)
+    qs = np.ascontiguousarray(w.batch.q_start, np.int32)
+    kd = np.ascontiguousarray(w.batch.row_kind, np.uint8)
+    fp8 = w.kv_dtype != "bf16"
+    p = fake_device_ptr
+    cpool = CPool(p, p, p if fp8 else None, p if fp8 else None, w.num_blocks, w.num_kv_heads,
+                  w.head_dim, 16, KV_FP8_E4M3 if fp8 else KV_BF16)
+    q = np.diff(qs)
+    cb = CBatch(int(sl.shape[0]), int(bt.shape[1]), int(qs[-1]),
+                int(q.max()) if len(q) else 1, int(sl.max()) if len(sl) else 1,
+                p, p, p, p, _np_ptr(bt), _np_ptr(sl), _np_ptr(qs), _np_ptr(kd))
+    return cpool, cb, (bt, sl, qs, kd)

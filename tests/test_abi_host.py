@@ -1,0 +1,168 @@
+"""Host-side checks of the C ABI: the library loads on a machine without a
+GPU, exports every symbol the header declares, and its validation and
+planning (pure host code) behave as documented.  No GPU work is enqueued:
+every call here either fails validation or is a host-only entry point."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+from paper_2504_03651_amd import echo
+from paper_2504_03651_amd import workload as W
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def test_library_exports_every_declared_symbol():
+    header = open(os.path.join(ROOT, "include", "echo.h")).read()
+    declared = set(re.findall(r"\b(echo_[a-z0-9_]+)\s*\(", header))
+    assert declared >= set(echo.SYMBOLS)
+    lib = ctypes.CDLL(echo.LIB_PATH)
+    for name in declared:
+        assert hasattr(lib, name), name
+
+
+def test_status_strings():
+    for code, name in [(0, "ECHO_OK"), (-1, "ECHO_E_INVALID"), (-3, "ECHO_E_ALIAS_WRITE"),
+                       (-6, "ECHO_E_HIP")]:
+        assert echo.status_string(code) == name
+
+
+def _structs(w):
+    return echo.host_structs(w)
+
+
+def test_valid_batches_pass_validation():
+    for w in (W.config1(), W.random_case(1), W.random_case(2, kv_dtype=W.KV_FP8)):
+        cp, cb, keep = _structs(w)
+        assert echo.validate(cp, cb, True) == echo.ECHO_OK, echo.last_error()
+        assert echo.validate(cp, cb, False) == echo.ECHO_OK
+
+
+def test_block_id_out_of_range():
+    w = W.config1()
+    w.batch.block_tables[1, 0] = w.num_blocks
+    cp, cb, keep = _structs(w)
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_RANGE
+    assert "outside" in echo.last_error()
+
+
+def test_decode_row_with_two_tokens():
+    w = W.config1()
+    w.batch.row_kind[1] = W.DECODE  # row 1 is a 32-token chunk
+    cp, cb, keep = _structs(w)
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+
+
+def test_append_into_aliased_block_is_rejected():
+    w = W.config1()
+    bt = w.batch.block_tables
+    # row 2 (decode, context 37) appends into its block 2; alias it from row 0
+    bt[0, 3] = bt[2, 2]
+    cp, cb, keep = _structs(w)
+    assert echo.validate(cp, cb, True) == echo.ECHO_E_ALIAS_WRITE
+    assert echo.validate(cp, cb, False) == echo.ECHO_OK  # attention alone may alias
+
+
+def test_two_rows_writing_one_block_is_rejected():
+    w = W.config1()
+    bt = w.batch.block_tables
+    bt[1, 0] = bt[3, 3]  # both prefill rows would write the same block
+    cp, cb, keep = _structs(w)
+    assert echo.validate(cp, cb, True) == echo.ECHO_E_ALIAS_WRITE
+
+
+def test_unsupported_head_dim_and_block_size():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    cp.head_dim = 96
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_UNSUPPORTED
+    cp.head_dim = 64
+    cp.block_size = 32
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_UNSUPPORTED
+
+
+def test_fp8_pool_needs_scales():
+    w = W.random_case(3, kv_dtype=W.KV_FP8)
+    cp, cb, keep = _structs(w)
+    cp.k_scale = None
+    assert echo.validate(cp, cb, True) == echo.ECHO_E_INVALID
+
+
+def test_q_start_must_start_at_zero_and_end_at_num_tokens():
+    w = W.config1()
+    cp, cb, (bt, sl, qs, kd) = _structs(w)
+    cb.num_tokens = cb.num_tokens + 1
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+    cb.num_tokens -= 1
+    qs[0] = 1
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+
+
+def test_partial_mirrors_rejected():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    cb.h_row_kind = None
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+
+
+def test_attention_without_mirrors_is_rejected_before_any_work():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    cb.h_block_tables = cb.h_seq_lens = cb.h_q_start = cb.h_row_kind = None
+    n = echo.lib().echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    assert n == 0 and "host mirrors" in echo.last_error()
+
+
+def test_block_copy_pair_rules():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    L = echo.lib()
+    for pairs, code in [([[3, 3]], echo.ECHO_E_INVALID),
+                        ([[1, 5], [2, 5]], echo.ECHO_E_INVALID),
+                        ([[1, 5], [5, 6]], echo.ECHO_E_INVALID),
+                        ([[1, 64]], echo.ECHO_E_RANGE),
+                        ([[-1, 2]], echo.ECHO_E_RANGE)]:
+        hp = np.ascontiguousarray(pairs, np.int32)
+        rc = L.echo_block_copy(ctypes.byref(cp), 0x1000, len(pairs),
+                               hp.ctypes.data_as(ctypes.c_void_p), None)
+        assert rc == code, (pairs, echo.last_error())
+
+
+def _unique_tokens(w):
+    used = {}
+    for r in range(w.batch.num_rows):
+        L = int(w.batch.seq_lens[r])
+        for j in range(0, L, 16):
+            b = int(w.batch.block_tables[r, j // 16])
+            used[b] = max(used.get(b, 0), min(16, L - j))
+    return sum(used.values())
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_plan_statistics(cfg):
+    w = W.config(cfg)
+    cp, cb, keep = _structs(w)
+    st = echo.plan_stats(cp, cb, w.num_q_heads)
+    assert st["unique_kv_tokens"] == _unique_tokens(w)
+    assert st["logical_kv_tokens"] == int(w.batch.seq_lens.sum())
+    q = np.diff(w.batch.q_start)
+    ctx = w.batch.seq_lens - q
+    assert st["causal_pairs"] == int((q * ctx + q * (q + 1) // 2).sum())
+    n_groups = len({r.group for r in w.rows if r.group >= 0 and r.kind == W.DECODE})
+    assert st["shared_segments"] >= n_groups
+    assert st["work_items"] == st["decode_items"] + st["prefill_items"]
+    assert st["workspace_bytes"] >= st["partial_slots"] * (w.head_dim + 1) * 4
+
+
+def test_plan_shares_prefix_blocks_in_config1():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    st = echo.plan_stats(cp, cb, w.num_q_heads)
+    # the two decode rows share one 2-block segment
+    assert st["shared_segments"] == 1
+    dup = W.config1(duplicate_prefix=True)
+    cp, cb, keep = _structs(dup)
+    assert echo.plan_stats(cp, cb, dup.num_q_heads)["shared_segments"] == 0

@@ -1,0 +1,174 @@
+"""GPU parity: the HIP path through the C ABI against the fp64 oracle.
+
+Append and block copy must match bit for bit (whole pools for small cases,
+every block the batch touches for full-size ones).  Attention outputs must
+stay within ATOL (max abs error) of the oracle: all outputs for small and
+fuzzed cases, sampled outputs at the five serving-shaped configurations.
+"""
+import numpy as np
+import pytest
+
+import oracle
+from paper_2504_03651_amd import workload as W
+from tests.gpu_util import ATOL, attn_error, compact, same_pool, sample_queries, say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch_cuda():
+    import torch
+    assert torch.cuda.is_available(), "no GPU"
+    from paper_2504_03651_amd import echo
+    echo.lib()
+    return torch
+
+
+def _run(w, torch, mirrors=True):
+    from paper_2504_03651_amd.session import Iteration
+    it = Iteration(w, mirrors=mirrors)
+    it.step()
+    torch.cuda.synchronize()
+    return it
+
+
+def _check_small(w, torch, label):
+    say(f"[case] {label}: rows={w.batch.num_rows} T={w.batch.num_tokens} "
+        f"Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} kv={w.kv_dtype}")
+    it = _run(w, torch)
+    pool, ref = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    got = it.out.cpu().numpy().reshape(ref.shape)
+    assert not np.isnan(got).any()
+    err, nerr = attn_error(got, ref)
+    say(f"       max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
+    return it, got
+
+
+def test_config1(torch_cuda):
+    _check_small(W.config1(), torch_cuda, "config1")
+
+
+def test_config1_prefix_shared_with_prefill_row(torch_cuda):
+    _check_small(W.config1(share_with_prefill=True), torch_cuda, "config1-share-prefill")
+
+
+FUZZ = [
+    # seed, rows, Hq, Hkv, D, kv, max_ctx, max_q
+    (101, 6, 8, 2, 128, W.KV_BF16, 600, 80),
+    (102, 8, 4, 4, 64, W.KV_BF16, 900, 40),
+    (103, 5, 8, 1, 128, W.KV_BF16, 500, 120),
+    (104, 7, 32, 8, 128, W.KV_BF16, 1200, 60),
+    (105, 6, 64, 8, 64, W.KV_BF16, 700, 50),
+    (106, 6, 8, 2, 128, W.KV_FP8, 600, 80),
+    (107, 6, 4, 4, 64, W.KV_FP8, 800, 33),
+    (108, 9, 16, 16, 128, W.KV_BF16, 5000, 300),
+    (109, 6, 32, 1, 128, W.KV_BF16, 400, 40),
+]
+
+
+@pytest.mark.parametrize("case", FUZZ, ids=[f"seed{c[0]}" for c in FUZZ])
+def test_fuzz(torch_cuda, case):
+    seed, rows, hq, hkv, d, kv, mc, mq = case
+    w = W.random_case(seed, num_rows=rows, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                      kv_dtype=kv, max_ctx=mc, max_q=mq, n_groups=2)
+    _check_small(w, torch_cuda, f"fuzz{seed}")
+
+
+def test_edge_rows(torch_cuda):
+    rows = [W.RowSpec(W.DECODE, 0, 1), W.RowSpec(W.DECODE, 16, 1, 0), W.RowSpec(W.DECODE, 17, 1, 0),
+            W.RowSpec(W.DECODE, 31, 1, 0), W.RowSpec(W.PREFILL, 0, 1), W.RowSpec(W.PREFILL, 15, 17),
+            W.RowSpec(W.PREFILL, 33, 300), W.RowSpec(W.DECODE, 1023, 1, 1),
+            W.RowSpec(W.DECODE, 1024, 1, 1), W.RowSpec(W.DECODE, 1025, 1, 1)]
+    w = W.build("edges", rows, {0: 16, 1: 1024}, 8, 2, 128, num_blocks=512, seed=9)
+    _check_small(w, torch_cuda, "edge-rows")
+
+
+def test_deterministic(torch_cuda):
+    w = W.random_case(110, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                      max_ctx=2000, max_q=64)
+    say("[case] determinism")
+    a = _run(w, torch_cuda).out.cpu().numpy()
+    b = _run(w, torch_cuda).out.cpu().numpy()
+    assert np.array_equal(a.view(np.uint32), b.view(np.uint32))
+
+
+def test_alias_vs_duplicate(torch_cuda):
+    a = W.random_case(111, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                      max_ctx=1500, max_q=40, n_groups=2)
+    b = W.random_case(111, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                      max_ctx=1500, max_q=40, n_groups=2, duplicate_prefix=True)
+    say("[case] alias vs duplicate")
+    ga = _run(a, torch_cuda).out.cpu().numpy()
+    gb = _run(b, torch_cuda).out.cpu().numpy()
+    assert np.abs(ga - gb).max() <= ATOL
+
+
+def test_empty_batch(torch_cuda):
+    from paper_2504_03651_amd import echo
+    say("[case] empty batch")
+    pool = echo.KVPool(16, 2, 64).poison()
+    empty = W.Batch(np.zeros((0, 1), np.int32), np.zeros(0, np.int32), np.zeros(1, np.int32),
+                    np.zeros(0, np.uint8))
+    b = echo.DeviceBatch(empty)
+    z = torch_cuda.zeros(1, dtype=torch_cuda.int16, device="cuda")
+    echo.kv_append(pool, b, z, z)
+    out = torch_cuda.zeros(1, dtype=torch_cuda.float32, device="cuda")
+    ws = torch_cuda.empty(256, dtype=torch_cuda.uint8, device="cuda")
+    echo.attn_mixed(pool, b, z, 4, 0.125, out, ws)
+    torch_cuda.cuda.synchronize()
+
+
+def test_append_without_mirrors(torch_cuda):
+    w = W.random_case(112, num_rows=6, head_dim=64, max_ctx=300, max_q=40)
+    from paper_2504_03651_amd.session import Iteration
+    say("[case] append without host mirrors")
+    it = Iteration(w, mirrors=False)
+    it.copy()
+    it.append()
+    torch_cuda.cuda.synchronize()
+    pool = oracle.prepare(w)
+    oracle.block_copy(pool, w.cow_pairs)
+    oracle.kv_append(pool, w.batch, w.k_new, w.v_new)
+    same_pool(it.pool_host(), pool)
+
+
+def test_block_copy_many_pairs(torch_cuda):
+    from paper_2504_03651_amd.session import Iteration
+    for kv in (W.KV_BF16, W.KV_FP8):
+        w = W.random_case(113, num_rows=5, head_dim=128, num_kv_heads=4, num_q_heads=8,
+                          kv_dtype=kv, max_ctx=500)
+        say(f"[case] block copy {kv}")
+        it = Iteration(w)
+        g = np.random.Generator(np.random.PCG64(5))
+        src = g.choice(w.used_blocks, size=min(40, len(w.used_blocks)), replace=False)
+        dst = g.choice(w.free_blocks, size=len(src), replace=False)
+        pairs = np.stack([src, dst], 1).astype(np.int32)
+        from paper_2504_03651_amd import echo
+        echo.block_copy(it.pool, torch_cuda.from_numpy(pairs).cuda(), pairs)
+        torch_cuda.cuda.synchronize()
+        pool = oracle.prepare(w)
+        oracle.block_copy(pool, pairs)
+        same_pool(it.pool_host(), pool)
+
+
+@pytest.mark.parametrize("cfg", [2, 3, 4, 5])
+def test_full_size_config(torch_cuda, cfg):
+    w = W.config(cfg)
+    say(f"[case] config{cfg} full size: rows={w.batch.num_rows} T={w.batch.num_tokens} "
+        f"NB={w.num_blocks} kv={w.kv_dtype}")
+    it = _run(w, torch_cuda)
+    c, ids = compact(w)
+    pool = oracle.prepare(c)
+    oracle.block_copy(pool, c.cow_pairs)
+    oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
+    say("       comparing touched blocks bit for bit")
+    same_pool(it.pool_host(ids), pool)
+    sel = sample_queries(w, 768, seed=cfg)
+    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, sel=sel)
+    got = it.out.cpu().numpy().reshape(-1, w.head_dim)[sel]
+    assert not np.isnan(it.out.cpu().numpy()).any()
+    err, nerr = attn_error(got, ref)
+    say(f"       {len(sel)} sampled outputs: max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
