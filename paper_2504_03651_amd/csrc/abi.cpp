@@ -176,8 +176,9 @@ int plan_for(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_
         return fail(ECHO_E_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
                     num_q_heads, pool->num_kv_heads);
     if (batch->num_rows == 0) {
-        plan = Plan{};
-        plan.merge_ptr.push_back(0);
+        plan.desc.clear();
+        plan.merge_ptr.assign(1, 0);
+        plan.layout = PlanLayout{};
         plan.layout.upload_words = 1;
         plan.layout.total_words = 64;
         return ECHO_OK;
@@ -357,12 +358,12 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
     int rc = plan_for(pool, batch, num_q_heads, plan);
     if (rc) return rc;
     std::memset(stats, 0, sizeof *stats);
-    stats->work_items = plan.layout.n_items;
+    stats->work_items = plan.layout.n_desc * plan.waves_per_desc;
     stats->decode_items = plan.stats.decode_items;
     stats->prefill_items = plan.stats.prefill_items;
     stats->shared_segments = plan.stats.shared_segments;
     stats->partial_slots = plan.layout.n_slots;
-    stats->merged_queries = plan.layout.n_merge;
+    stats->merged_queries = plan.layout.n_merge_rows * num_q_heads;
     stats->logical_kv_tokens = plan.stats.logical_kv_tokens;
     stats->causal_pairs = plan.stats.causal_pairs;
     stats->workspace_bytes = plan.layout.total_words * 4;
@@ -401,8 +402,12 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     const PlanLayout &L = plan.layout;
     int32_t *w = (int32_t *)workspace;
     AttnArgs a;
-    a.items = (const AttnItem *)(w + L.off_items);
-    a.n_items = (int32_t)L.n_items;
+    a.desc = (const WorkDesc *)(w + L.off_desc);
+    a.n_waves = L.n_desc * plan.waves_per_desc;
+    a.waves_per_desc = plan.waves_per_desc;
+    a.head_chunks = plan.head_chunks;
+    a.heads_per_chunk = plan.heads_per_chunk;
+    a.group = num_q_heads / pool->num_kv_heads;
     a.tok_list = w + L.off_tok_list;
     a.klim = w + L.off_klim;
     a.q = (const uint16_t *)q;
@@ -419,10 +424,15 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     a.part_o = (float *)(w + L.off_part_o);
     a.part_lse = (float *)(w + L.off_part_lse);
     MergeArgs m;
-    m.n_merge = (int32_t)L.n_merge;
-    m.merge_q = w + L.off_merge_q;
+    m.n_waves = L.n_merge_rows * num_q_heads;
+    m.num_q_heads = num_q_heads;
+    m.head_chunks = plan.head_chunks;
+    m.heads_per_chunk = plan.heads_per_chunk;
+    m.group = a.group;
+    m.desc = a.desc;
+    m.merge_tok = w + L.off_merge_tok;
     m.merge_ptr = w + L.off_merge_ptr;
-    m.merge_slot = w + L.off_merge_slot;
+    m.merge_ent = w + L.off_merge_ent;
     m.part_o = a.part_o;
     m.part_lse = a.part_lse;
     m.out = out;

@@ -3,8 +3,9 @@
 //   append_kernel       scatter new K/V into the paged pool (bf16 bit copy,
 //                       or e4m3 quantisation with per-(block, head) scales)
 //   block_copy_kernel   whole-block copy-on-write
-//   attn_items_kernel   one wave per work item: up to 16 query vectors against
-//                       a run of 16-token blocks, online softmax, bf16 MFMA
+//   attn_kernel         one wave per (work descriptor, KV head, head chunk): up
+//                       to 16 query vectors against a run of 16-token blocks,
+//                       online softmax, bf16 MFMA
 //   merge_kernel        log-sum-exp merge of split / segment partial results
 //
 // MFMA tile orientation (v_mfma_f32_16x16x32_bf16, wave64):
@@ -220,7 +221,7 @@ struct KV<true> {
 };
 
 template <int D, bool FP8>
-__global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
     typedef typename kv::Raw Raw;
@@ -229,21 +230,26 @@ __global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int idx = blockIdx.x * 4 + wave;
-    if (idx >= a.n_items) return;
-    const int32_t *ip = (const int32_t *)(a.items + idx);
+    const int64_t idx = (int64_t)blockIdx.x * 4 + wave;
+    if (idx >= a.n_waves) return;
+    const int di = (int)(idx / a.waves_per_desc);
+    const int rem = (int)(idx - (int64_t)di * a.waves_per_desc);
+    const int kvh = rem / a.head_chunks;
+    const int hc = rem - kvh * a.head_chunks;
+    const int32_t *ip = (const int32_t *)(a.desc + di);
     const int tok_off = __builtin_amdgcn_readfirstlane(ip[0]);
     const int shape = __builtin_amdgcn_readfirstlane(ip[1]);
-    const int h0 = __builtin_amdgcn_readfirstlane(ip[2]);
-    const int kvh = __builtin_amdgcn_readfirstlane(ip[3]);
-    const int bt_row = __builtin_amdgcn_readfirstlane(ip[4]);
-    const int key_begin = __builtin_amdgcn_readfirstlane(ip[5]);
-    const int key_end = __builtin_amdgcn_readfirstlane(ip[6]);
-    const int part = __builtin_amdgcn_readfirstlane(ip[7]);
+    const int bt_row = __builtin_amdgcn_readfirstlane(ip[2]);
+    const int key_begin = __builtin_amdgcn_readfirstlane(ip[3]);
+    const int key_end = __builtin_amdgcn_readfirstlane(ip[4]);
+    const int dpart = __builtin_amdgcn_readfirstlane(ip[5]);
+    const int nt = shape & 0xFF;
+    const int h0 = kvh * a.group + hc * 16;
+    const int nh = min(a.heads_per_chunk, a.group - hc * 16);
+    const int part = dpart < 0 ? -1 : dpart + rem * nt * a.heads_per_chunk;
 
     const int g4 = lane >> 4;   // 16-lane group: selects 8 of each 32 k-values
     const int c16 = lane & 15;  // MFMA row (A) / column (B, C) index
-    const int nt = shape & 0xFF, nh = (shape >> 8) & 0xFF;
     const int qi = c16 / nh, qj = c16 - (c16 / nh) * nh;
     const bool qvalid = qi < nt;
     int tok = 0, klim = 0;
@@ -379,28 +385,44 @@ __global__ __launch_bounds__(256) void attn_items_kernel(AttnArgs a) {
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const int lane = threadIdx.x & 63;
-    const int m = blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (m >= a.n_merge) return;
-    const int q = a.merge_q[m];
-    const int s0 = a.merge_ptr[m], s1 = a.merge_ptr[m + 1];
+    const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (m >= a.n_waves) return;
+    const int row = (int)(m / a.num_q_heads);
+    const int h = (int)(m - (int64_t)row * a.num_q_heads);
+    const int tok = a.merge_tok[row];
+    const int e0 = a.merge_ptr[row], e1 = a.merge_ptr[row + 1];
+    // where head h of a slice's query i lands inside a descriptor's slots
+    const int kvh = h / a.group;
+    const int hc = (h - kvh * a.group) / 16;
+    const int jh = h - kvh * a.group - hc * 16;
+    const int nh = min(a.heads_per_chunk, a.group - hc * 16);
+    const int rem = kvh * a.head_chunks + hc;
     float mx = -INFINITY;
-    for (int s = s0; s < s1; ++s) mx = fmaxf(mx, a.part_lse[a.merge_slot[s]]);
+    for (int e = e0; e < e1; ++e) {
+        const WorkDesc *d = a.desc + a.merge_ent[2 * e];
+        const int slot = d->part + rem * (d->shape & 0xFF) * a.heads_per_chunk +
+                         a.merge_ent[2 * e + 1] * nh + jh;
+        mx = fmaxf(mx, a.part_lse[slot]);
+    }
     constexpr int PER = D / 64;
     float acc[PER];
 #pragma unroll
-    for (int e = 0; e < PER; ++e) acc[e] = 0.f;
+    for (int k = 0; k < PER; ++k) acc[k] = 0.f;
     float wsum = 0.f;
-    for (int s = s0; s < s1; ++s) {
-        const int slot = a.merge_slot[s];
+    for (int e = e0; e < e1; ++e) {
+        const WorkDesc *d = a.desc + a.merge_ent[2 * e];
+        const int slot = d->part + rem * (d->shape & 0xFF) * a.heads_per_chunk +
+                         a.merge_ent[2 * e + 1] * nh + jh;
         const float lse = a.part_lse[slot];
         const float w = lse == -INFINITY ? 0.f : exp2f(lse - mx);
         wsum += w;
 #pragma unroll
-        for (int e = 0; e < PER; ++e) acc[e] += w * a.part_o[(int64_t)slot * D + lane * PER + e];
+        for (int k = 0; k < PER; ++k) acc[k] += w * a.part_o[(int64_t)slot * D + lane * PER + k];
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
+    float *o = a.out + ((int64_t)tok * a.num_q_heads + h) * D + lane * PER;
 #pragma unroll
-    for (int e = 0; e < PER; ++e) a.out[(int64_t)q * D + lane * PER + e] = acc[e] * inv;
+    for (int k = 0; k < PER; ++k) o[k] = acc[k] * inv;
 }
 
 // ------------------------------------------------------------------ launchers
@@ -424,17 +446,17 @@ hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s) {
 
 hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, int head_dim, bool fp8,
                             hipStream_t s) {
-    if (a.n_items > 0) {
-        const dim3 grid((unsigned)((a.n_items + 3) / 4)), block(256);
-        if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_items_kernel<64, false>), grid, block, 0, s, a);
-        else if (head_dim == 64) hipLaunchKernelGGL((attn_items_kernel<64, true>), grid, block, 0, s, a);
-        else if (!fp8) hipLaunchKernelGGL((attn_items_kernel<128, false>), grid, block, 0, s, a);
-        else hipLaunchKernelGGL((attn_items_kernel<128, true>), grid, block, 0, s, a);
+    if (a.n_waves > 0) {
+        const dim3 grid((unsigned)((a.n_waves + 3) / 4)), block(256);
+        if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, a);
+        else if (head_dim == 64) hipLaunchKernelGGL((attn_kernel<64, true>), grid, block, 0, s, a);
+        else if (!fp8) hipLaunchKernelGGL((attn_kernel<128, false>), grid, block, 0, s, a);
+        else hipLaunchKernelGGL((attn_kernel<128, true>), grid, block, 0, s, a);
         hipError_t e = hipGetLastError();
         if (e != hipSuccess) return e;
     }
-    if (m.n_merge > 0) {
-        const dim3 grid((unsigned)((m.n_merge + 3) / 4)), block(256);
+    if (m.n_waves > 0) {
+        const dim3 grid((unsigned)((m.n_waves + 3) / 4)), block(256);
         if (head_dim == 64) hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, s, m);
         else hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, s, m);
         return hipGetLastError();

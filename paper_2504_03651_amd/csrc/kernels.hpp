@@ -27,8 +27,10 @@ struct BlockCopyArgs {
 };
 
 struct AttnArgs {
-    const AttnItem *items;
-    int32_t n_items;
+    const WorkDesc *desc;
+    int64_t n_waves;                // n_desc * waves_per_desc
+    int32_t waves_per_desc;         // num_kv_heads * head_chunks
+    int32_t head_chunks, heads_per_chunk, group;  // group = Hq / Hkv
     const int32_t *tok_list, *klim;
     const uint16_t *q;              // [T][Hq][D] bf16 bits
     int32_t num_q_heads, num_kv_heads;
@@ -41,8 +43,10 @@ struct AttnArgs {
 };
 
 struct MergeArgs {
-    int32_t n_merge;
-    const int32_t *merge_q, *merge_ptr, *merge_slot;
+    int64_t n_waves;                // merged rows * Hq
+    int32_t num_q_heads, head_chunks, heads_per_chunk, group;
+    const WorkDesc *desc;
+    const int32_t *merge_tok, *merge_ptr, *merge_ent;
     const float *part_o, *part_lse;
     float *out;
 };

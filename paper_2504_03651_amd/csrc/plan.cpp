@@ -75,29 +75,39 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
                Plan &plan) {
     const int32_t B = b.num_rows, T = b.num_tokens;
     const int32_t G = Hq / Hkv;
-    const int32_t nh_full = G < kWaveQueries ? G : kWaveQueries;
-    const int32_t n_head_chunks = (G + kWaveQueries - 1) / kWaveQueries;
+    const int32_t hpc = G < kWaveQueries ? G : kWaveQueries;   // heads per chunk
+    const int32_t nhc = (G + kWaveQueries - 1) / kWaveQueries; // head chunks
+    const int32_t nt_max = kWaveQueries / hpc;                 // tokens per slice
     const int32_t split = opt.split_blocks > 0 ? opt.split_blocks : 32;
+    plan.head_chunks = nhc;
+    plan.heads_per_chunk = hpc;
+    plan.waves_per_desc = Hkv * nhc;
 
-    plan.items.clear();
+    plan.desc.clear();
     plan.tok_list.clear();
-    plan.merge_q.clear();
+    plan.merge_tok.clear();
     plan.merge_ptr.clear();
-    plan.merge_slot.clear();
-    plan.klim.assign((size_t)T, 0);
+    plan.merge_ent.clear();
+    plan.klim.resize((size_t)T);
     plan.stats = PlanStats{};
 
     // keys visible to every new token: its position + 1
     for (int32_t r = 0; r < B; ++r) {
         const int32_t q = b.q_start[r + 1] - b.q_start[r];
         const int32_t c = b.seq_lens[r] - q;
-        for (int32_t i = 0; i < q; ++i) plan.klim[(size_t)b.q_start[r] + i] = c + i + 1;
+        int32_t *kl = plan.klim.data() + b.q_start[r];
+        for (int32_t i = 0; i < q; ++i) kl[i] = c + i + 1;
         plan.stats.logical_kv_tokens += b.seq_lens[r];
         plan.stats.causal_pairs += (int64_t)q * c + (int64_t)q * (q + 1) / 2;
     }
 
     // ---- decode rows: segments from the trie plus one private tail per row
-    std::vector<int32_t> nro((size_t)B, 0), R, tail_start((size_t)B, 0), seg_rows;
+    std::vector<int32_t> &nro = plan.nro, &R = plan.rows, &tail_start = plan.tail_start,
+                         &seg_rows = plan.seg_rows;
+    nro.assign((size_t)B, 0);
+    tail_start.assign((size_t)B, 0);
+    R.clear();
+    seg_rows.clear();
     std::vector<Segment> segs;
     for (int32_t r = 0; r < B; ++r) {
         if (b.kind[r] != ECHO_ROW_DECODE) continue;
@@ -106,7 +116,6 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     }
     build_trie(b, nro, R, tail_start, segs, seg_rows);
     plan.stats.shared_segments = (int64_t)segs.size();
-    const size_t n_shared = segs.size();
     for (int32_t r : R) {
         Segment s;
         s.rows_off = (int32_t)seg_rows.size();
@@ -119,28 +128,28 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     }
 
     // contributions per decode row: sum over its segments of their splits
-    std::vector<int32_t> cnt((size_t)B, 0);
+    std::vector<int32_t> &cnt = plan.cnt, &moff = plan.moff, &cursor = plan.cursor;
+    cnt.assign((size_t)B, 0);
     auto n_splits = [&](const Segment &s) { return (s.j1 - s.j0 + split - 1) / split; };
     for (const Segment &s : segs)
         for (int32_t k = 0; k < s.nrows; ++k) cnt[seg_rows[s.rows_off + k]] += n_splits(s);
 
-    // merge list layout: rows with more than one contribution, all heads
-    std::vector<int32_t> moff((size_t)B, -1), cursor;
-    int64_t n_merge_slots = 0;
+    // merge lists: rows with more than one contribution; entries (desc, i)
+    moff.assign((size_t)B, -1);
+    int64_t n_ent = 0;
     for (int32_t r : R) {
         if (cnt[r] < 2) continue;
-        moff[r] = (int32_t)plan.merge_q.size();
-        for (int32_t h = 0; h < Hq; ++h) {
-            plan.merge_q.push_back(b.q_start[r] * Hq + h);
-            plan.merge_ptr.push_back((int32_t)n_merge_slots);
-            n_merge_slots += cnt[r];
-        }
+        moff[r] = (int32_t)plan.merge_tok.size();
+        plan.merge_tok.push_back(b.q_start[r]);
+        plan.merge_ptr.push_back((int32_t)n_ent);
+        n_ent += cnt[r];
     }
-    plan.merge_ptr.push_back((int32_t)n_merge_slots);
-    plan.merge_slot.assign((size_t)n_merge_slots, -1);
-    cursor.assign(plan.merge_q.size(), 0);
+    plan.merge_ptr.push_back((int32_t)n_ent);
+    plan.merge_ent.assign((size_t)(2 * n_ent), -1);
+    cursor.assign(plan.merge_tok.size(), 0);
 
     int64_t n_slots = 0;
+    const int64_t wpd = plan.waves_per_desc;
     for (size_t si = 0; si < segs.size(); ++si) {
         const Segment &s = segs[si];
         const int32_t tok_base = (int32_t)plan.tok_list.size();
@@ -149,48 +158,34 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         const int32_t rep = seg_rows[s.rows_off];
         const bool direct = (s.nrows == 1 && cnt[rep] == 1);
         for (int32_t j = s.j0; j < s.j1; j += split) {
-            const int32_t kb = kBlock * j;
             const int32_t jend = std::min(j + split, s.j1);
-            const int32_t ke = std::min(kBlock * jend, s.key_end);
-            for (int32_t g = 0; g < Hkv; ++g) {
-                for (int32_t hc = 0; hc < n_head_chunks; ++hc) {
-                    const int32_t h0 = g * G + hc * kWaveQueries;
-                    const int32_t nh = std::min(nh_full, G - hc * kWaveQueries);
-                    const int32_t nt = kWaveQueries / nh;
-                    for (int32_t k0 = 0; k0 < s.nrows; k0 += nt) {
-                        const int32_t ntk = std::min(nt, s.nrows - k0);
-                        AttnItem it;
-                        it.tok_off = tok_base + k0;
-                        it.shape = ntk | (nh << 8);
-                        it.h0 = h0;
-                        it.kvh = g;
-                        it.bt_row = rep;
-                        it.key_begin = kb;
-                        it.key_end = ke;
-                        it.part = -1;
-                        if (!direct) {
-                            it.part = (int32_t)n_slots;
-                            for (int32_t i = 0; i < ntk; ++i) {
-                                const int32_t r = seg_rows[s.rows_off + k0 + i];
-                                for (int32_t jh = 0; jh < nh; ++jh) {
-                                    const int32_t m = moff[r] + h0 + jh;
-                                    plan.merge_slot[(size_t)plan.merge_ptr[m] + cursor[m]++] =
-                                        (int32_t)(n_slots + i * nh + jh);
-                                }
-                            }
-                            n_slots += (int64_t)ntk * nh;
-                        }
-                        plan.items.push_back(it);
-                        ++plan.stats.decode_items;
+            for (int32_t k0 = 0; k0 < s.nrows; k0 += nt_max) {
+                const int32_t ntk = std::min(nt_max, s.nrows - k0);
+                WorkDesc d;
+                d.tok_off = tok_base + k0;
+                d.shape = ntk;
+                d.bt_row = rep;
+                d.key_begin = kBlock * j;
+                d.key_end = std::min(kBlock * jend, s.key_end);
+                d.part = -1;
+                d.pad0 = d.pad1 = 0;
+                if (!direct) {
+                    d.part = (int32_t)n_slots;
+                    const int32_t di = (int32_t)plan.desc.size();
+                    for (int32_t i = 0; i < ntk; ++i) {
+                        const int32_t m = moff[seg_rows[s.rows_off + k0 + i]];
+                        const int64_t e = plan.merge_ptr[m] + cursor[m]++;
+                        plan.merge_ent[2 * e] = di;
+                        plan.merge_ent[2 * e + 1] = i;
                     }
+                    n_slots += wpd * ntk * hpc;
                 }
+                plan.desc.push_back(d);
+                plan.stats.decode_items += wpd;
             }
         }
-        if (si < n_shared) plan.stats.unique_kv_tokens += (int64_t)kBlock * (s.j1 - s.j0);
-        else plan.stats.unique_kv_tokens += s.key_end - kBlock * s.j0;
     }
-
-    for (int32_t v : plan.merge_slot)
+    for (int32_t v : plan.merge_ent)
         if (v < 0) return ECHO_E_INVALID;  // every merged result must have all its parts
 
     // ---- prefill rows: consecutive token slices, whole causal key range
@@ -198,61 +193,61 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         if (b.kind[r] != ECHO_ROW_PREFILL) continue;
         const int32_t q = b.q_start[r + 1] - b.q_start[r];
         const int32_t c = b.seq_lens[r] - q;
-        plan.stats.unique_kv_tokens += b.seq_lens[r];
-        for (int32_t g = 0; g < Hkv; ++g) {
-            for (int32_t hc = 0; hc < n_head_chunks; ++hc) {
-                const int32_t h0 = g * G + hc * kWaveQueries;
-                const int32_t nh = std::min(nh_full, G - hc * kWaveQueries);
-                const int32_t nt = kWaveQueries / nh;
-                for (int32_t i0 = 0; i0 < q; i0 += nt) {
-                    const int32_t ntk = std::min(nt, q - i0);
-                    AttnItem it;
-                    it.tok_off = b.q_start[r] + i0;
-                    it.shape = ntk | (nh << 8) | kItemConsecutive;
-                    it.h0 = h0;
-                    it.kvh = g;
-                    it.bt_row = r;
-                    it.key_begin = 0;
-                    it.key_end = c + i0 + ntk;
-                    it.part = -1;
-                    plan.items.push_back(it);
-                    ++plan.stats.prefill_items;
-                }
-            }
+        for (int32_t i0 = 0; i0 < q; i0 += nt_max) {
+            const int32_t ntk = std::min(nt_max, q - i0);
+            WorkDesc d;
+            d.tok_off = b.q_start[r] + i0;
+            d.shape = ntk | kItemConsecutive;
+            d.bt_row = r;
+            d.key_begin = 0;
+            d.key_end = c + i0 + ntk;
+            d.part = -1;
+            d.pad0 = d.pad1 = 0;
+            plan.desc.push_back(d);
+            plan.stats.prefill_items += wpd;
         }
     }
 
-    // heavy items first (counting sort on 32-key steps, stable)
+    // heavy descriptors first (counting sort on 32-key steps, stable)
     {
         const int32_t nb = 1024;
-        std::vector<int32_t> count(nb + 1, 0);
-        auto bucket = [&](const AttnItem &it) {
-            int32_t steps = (it.key_end - it.key_begin + 31) / 32;
+        std::vector<int32_t> &count = plan.bucket;
+        count.assign(nb + 1, 0);
+        auto bucket = [&](const WorkDesc &d) {
+            int32_t steps = (d.key_end - d.key_begin + 31) / 32;
             return nb - 1 - std::min(steps, nb - 1);
         };
-        for (const AttnItem &it : plan.items) ++count[bucket(it) + 1];
+        for (const WorkDesc &d : plan.desc) ++count[bucket(d) + 1];
         for (int32_t i = 0; i < nb; ++i) count[i + 1] += count[i];
-        std::vector<AttnItem> sorted(plan.items.size());
-        for (const AttnItem &it : plan.items) sorted[count[bucket(it)]++] = it;
-        plan.items.swap(sorted);
+        // merge entries name descriptors by index: remap them after sorting
+        std::vector<int32_t> &where = plan.cursor;
+        where.resize(plan.desc.size());
+        plan.desc_sorted.resize(plan.desc.size());
+        for (size_t i = 0; i < plan.desc.size(); ++i) {
+            const int32_t pos = count[bucket(plan.desc[i])]++;
+            plan.desc_sorted[pos] = plan.desc[i];
+            where[i] = pos;
+        }
+        plan.desc.swap(plan.desc_sorted);
+        for (int64_t e = 0; e < n_ent; ++e) plan.merge_ent[2 * e] = where[plan.merge_ent[2 * e]];
     }
 
     PlanLayout &L = plan.layout;
     L = PlanLayout{};
     L.head_dim = D;
-    L.n_items = (int64_t)plan.items.size();
+    L.n_desc = (int64_t)plan.desc.size();
     L.n_tok_list = (int64_t)plan.tok_list.size();
     L.n_tokens = T;
-    L.n_merge = (int64_t)plan.merge_q.size();
-    L.n_merge_slots = n_merge_slots;
+    L.n_merge_rows = (int64_t)plan.merge_tok.size();
+    L.n_merge_entries = n_ent;
     L.n_slots = n_slots;
     int64_t w = 0;
-    L.off_items = w;      w += L.n_items * 8;
+    L.off_desc = w;       w += L.n_desc * 8;
     L.off_tok_list = w;   w += L.n_tok_list;
     L.off_klim = w;       w += L.n_tokens;
-    L.off_merge_q = w;    w += L.n_merge;
-    L.off_merge_ptr = w;  w += L.n_merge + 1;
-    L.off_merge_slot = w; w += L.n_merge_slots;
+    L.off_merge_tok = w;  w += L.n_merge_rows;
+    L.off_merge_ptr = w;  w += L.n_merge_rows + 1;
+    L.off_merge_ent = w;  w += 2 * n_ent;
     L.upload_words = w;
     w = align_words(w, 64);
     L.off_part_lse = w;   w += n_slots;
@@ -265,14 +260,15 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
 void pack_plan(const Plan &plan, void *dst) {
     const PlanLayout &L = plan.layout;
     int32_t *w = static_cast<int32_t *>(dst);
-    if (L.n_items) std::memcpy(w + L.off_items, plan.items.data(), L.n_items * sizeof(AttnItem));
+    if (L.n_desc) std::memcpy(w + L.off_desc, plan.desc.data(), L.n_desc * sizeof(WorkDesc));
     if (L.n_tok_list)
         std::memcpy(w + L.off_tok_list, plan.tok_list.data(), L.n_tok_list * 4);
     if (L.n_tokens) std::memcpy(w + L.off_klim, plan.klim.data(), L.n_tokens * 4);
-    if (L.n_merge) std::memcpy(w + L.off_merge_q, plan.merge_q.data(), L.n_merge * 4);
-    std::memcpy(w + L.off_merge_ptr, plan.merge_ptr.data(), (L.n_merge + 1) * 4);
-    if (L.n_merge_slots)
-        std::memcpy(w + L.off_merge_slot, plan.merge_slot.data(), L.n_merge_slots * 4);
+    if (L.n_merge_rows)
+        std::memcpy(w + L.off_merge_tok, plan.merge_tok.data(), L.n_merge_rows * 4);
+    std::memcpy(w + L.off_merge_ptr, plan.merge_ptr.data(), (L.n_merge_rows + 1) * 4);
+    if (L.n_merge_entries)
+        std::memcpy(w + L.off_merge_ent, plan.merge_ent.data(), L.n_merge_entries * 8);
 }
 
 }  // namespace echo

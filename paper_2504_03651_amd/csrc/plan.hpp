@@ -20,36 +20,43 @@ constexpr int kBlock = 16;
 constexpr int kWaveQueries = 16;   // query vectors per wave (MFMA N dimension)
 constexpr int kWavesPerGroup = 4;  // waves per workgroup
 
-// flags in AttnItem::shape
+// flags in WorkDesc::shape
 constexpr int32_t kItemConsecutive = 1 << 16;  // tokens tok_off, tok_off+1, ...
 
-struct AttnItem {      // 32 bytes
+// One key range of one block table against one slice of query tokens.  On
+// the GPU it expands into num_kv_heads * head_chunks waves (a head chunk is
+// up to 16 query heads of one KV head), so the host never enumerates heads.
+struct WorkDesc {      // 32 bytes
     int32_t tok_off;   // first token, or offset into the plan's token list
-    int32_t shape;     // nt | nh << 8 | flags
-    int32_t h0;        // first query head
-    int32_t kvh;       // KV head
+    int32_t shape;     // nt | flags: nt tokens in the slice
     int32_t bt_row;    // row whose block table supplies the block ids
     int32_t key_begin; // first key position, a multiple of 16
     int32_t key_end;   // one past the last key position
     int32_t part;      // first partial slot, or -1: write `out` directly
+    int32_t pad0, pad1;
 };
-static_assert(sizeof(AttnItem) == 32, "item layout");
+static_assert(sizeof(WorkDesc) == 32, "descriptor layout");
+
+// Wave w of the attention grid handles descriptor w / (Hkv * head_chunks),
+// KV head (w % (Hkv * head_chunks)) / head_chunks and head chunk
+// w % head_chunks; its partial slots start at
+// part + (w % (Hkv * head_chunks)) * nt * heads_per_chunk.
 
 // Offsets (in 4-byte words from the start of the workspace) of each region.
 struct PlanLayout {
-    int64_t n_items = 0;
+    int64_t n_desc = 0;
     int64_t n_tok_list = 0;
     int64_t n_tokens = 0;
-    int64_t n_merge = 0;
-    int64_t n_merge_slots = 0;
+    int64_t n_merge_rows = 0;
+    int64_t n_merge_entries = 0;
     int64_t n_slots = 0;
     int32_t head_dim = 0;
-    int64_t off_items = 0;      // AttnItem[n_items]
+    int64_t off_desc = 0;       // WorkDesc[n_desc]
     int64_t off_tok_list = 0;   // int32[n_tok_list]
     int64_t off_klim = 0;       // int32[n_tokens]: keys visible to each token
-    int64_t off_merge_q = 0;    // int32[n_merge]: t * Hq + h
-    int64_t off_merge_ptr = 0;  // int32[n_merge + 1]
-    int64_t off_merge_slot = 0; // int32[n_merge_slots]
+    int64_t off_merge_tok = 0;  // int32[n_merge_rows]: the row's token
+    int64_t off_merge_ptr = 0;  // int32[n_merge_rows + 1]
+    int64_t off_merge_ent = 0;  // int32[2 * n_merge_entries]: (descriptor, index in slice)
     int64_t upload_words = 0;   // everything above is uploaded
     int64_t off_part_lse = 0;   // float[n_slots]
     int64_t off_part_o = 0;     // float[n_slots][head_dim]
@@ -58,7 +65,7 @@ struct PlanLayout {
 
 struct PlanStats {
     int64_t decode_items = 0, prefill_items = 0, shared_segments = 0;
-    int64_t unique_kv_tokens = 0, logical_kv_tokens = 0, causal_pairs = 0;
+    int64_t logical_kv_tokens = 0, causal_pairs = 0;
 };
 
 struct HostBatch {
@@ -73,10 +80,15 @@ struct PlanOptions {
 
 // Host plan under construction (reused between calls on the same thread).
 struct Plan {
-    std::vector<AttnItem> items;
-    std::vector<int32_t> tok_list, klim, merge_q, merge_ptr, merge_slot;
+    std::vector<WorkDesc> desc, desc_sorted;
+    std::vector<int32_t> tok_list, klim, merge_tok, merge_ptr, merge_ent;
+    // scratch
+    std::vector<int32_t> nro, rows, tail_start, seg_rows, cnt, moff, cursor, bucket;
     PlanLayout layout;
     PlanStats stats;
+    int32_t waves_per_desc = 1;   // num_kv_heads * head_chunks
+    int32_t head_chunks = 1;
+    int32_t heads_per_chunk = 1;  // min(G, 16)
 };
 
 // Builds the plan for a validated batch.  Returns 0 or an echo_status_t.
