@@ -175,6 +175,8 @@ int plan_for(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_
     if (num_q_heads <= 0 || num_q_heads % pool->num_kv_heads != 0)
         return fail(ECHO_E_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
                     num_q_heads, pool->num_kv_heads);
+    if (num_q_heads / pool->num_kv_heads > kPrefillQueries)
+        return fail(ECHO_E_UNSUPPORTED, "more than %d query heads per KV head", kPrefillQueries);
     if (batch->num_rows == 0) {
         plan.desc.clear();
         plan.merge_ptr.assign(1, 0);
@@ -436,7 +438,25 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     m.part_o = a.part_o;
     m.part_lse = a.part_lse;
     m.out = out;
-    hipError_t e = launch_attention(a, m, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s);
+    PrefillArgs pf;
+    pf.pdesc = (const PrefillDesc *)(w + L.off_pdesc);
+    pf.n_pdesc = (int32_t)L.n_pdesc;
+    pf.n_logical = (int32_t)(L.n_pdesc * pool->num_kv_heads);
+    pf.per_xcd = (pf.n_logical + 7) / 8;
+    pf.group = a.group;
+    pf.klim = a.klim;
+    pf.q = a.q;
+    pf.num_q_heads = num_q_heads;
+    pf.num_kv_heads = pool->num_kv_heads;
+    pf.k = pool->k;
+    pf.v = pool->v;
+    pf.k_scale = pool->k_scale;
+    pf.v_scale = pool->v_scale;
+    pf.block_tables = batch->block_tables;
+    pf.max_blocks_per_row = batch->max_blocks_per_row;
+    pf.scale_log2 = a.scale_log2;
+    pf.out = out;
+    hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s);
     if (e != hipSuccess) return hip_fail(e, "attention launch");
     return ECHO_OK;
 }

@@ -380,6 +380,235 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i + 4 * g4) = acc[i] * inv;
 }
 
+// ------------------------------------------------------------------ prefill
+//
+// One workgroup = 4 waves x 32 query vectors (consecutive tokens of one
+// prefill chunk x the query heads of one KV head).  K/V tiles of 64 keys are
+// gathered block by block into double-buffered LDS (bf16; e4m3 is widened on
+// the way in) and shared by the four waves.  Row padding of 16 bytes keeps
+// the 16-byte MFMA operand reads free of bank conflicts.
+
+constexpr int kPfKeys = 64;
+
+template <int D>
+struct PfLds {
+    static constexpr int KROW = D + 8;          // bf16 elements per K row
+    static constexpr int VROW = kPfKeys + 8;    // bf16 elements per V^T row
+    static constexpr int KSZ = kPfKeys * KROW;
+    static constexpr int VSZ = D * VROW;
+    static constexpr int STAGE = KSZ + VSZ;
+    static constexpr int BYTES = 2 * STAGE * 2 + 2 * 8 * 4;  // two stages + scales
+};
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+    typedef KV<FP8> kv;
+    typedef typename kv::T KT;
+    typedef typename kv::Raw Raw;
+    typedef PfLds<D> LD;
+    constexpr int NC = D / 32, NT = D / 16;
+    constexpr int LPT = D / 32;                 // 8-element loads per thread per tile (K and V each)
+    extern __shared__ __align__(16) uint16_t lds[];
+    float *lscale = (float *)(lds + 2 * LD::STAGE);  // [2 stages][k 4 | v 4]
+
+    const int P = blockIdx.x;
+    const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
+    if (L >= a.n_logical) return;
+    const int kvh = L / a.n_pdesc;
+    const int di = L - kvh * a.n_pdesc;
+    const int32_t *dp = (const int32_t *)(a.pdesc + di);
+    const int row = __builtin_amdgcn_readfirstlane(dp[0]);
+    const int tok0 = __builtin_amdgcn_readfirstlane(dp[1]);
+    const int ntok = __builtin_amdgcn_readfirstlane(dp[2]);
+    const int key_end = __builtin_amdgcn_readfirstlane(dp[3]);
+
+    const int tid = threadIdx.x;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int g4 = lane >> 4, c16 = lane & 15;
+    const int G = a.group;
+
+    // this lane's two query columns (N tiles nn = 0, 1)
+    bf16x8_t qf[2][NC];
+    int klim[2], qtok[2], qhead[2];
+    bool qok[2];
+#pragma unroll
+    for (int nn = 0; nn < 2; ++nn) {
+        const int qi = 32 * wave + 16 * nn + c16;
+        const int tl = qi / G;
+        qok[nn] = tl < ntok;
+        qtok[nn] = tok0 + (qok[nn] ? tl : 0);
+        qhead[nn] = kvh * G + (qi - tl * G);
+        klim[nn] = qok[nn] ? a.klim[qtok[nn]] : 0;
+        const uint16_t *qp = a.q + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 8 * g4;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+            u32x4_t w = {0u, 0u, 0u, 0u};
+            if (qok[nn]) w = *(const u32x4_t *)(qp + 32 * c);
+            qf[nn][c] = __builtin_bit_cast(bf16x8_t, w);
+        }
+    }
+
+    f32x4_t acc[2][NT];
+#pragma unroll
+    for (int nn = 0; nn < 2; ++nn)
+#pragma unroll
+        for (int i = 0; i < NT; ++i) acc[nn][i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+
+    const int32_t *btr = a.block_tables + (int64_t)row * a.max_blocks_per_row;
+    const int64_t blk_stride = (int64_t)a.num_kv_heads * 16 * D;
+    const KT *kbase = (const KT *)a.k + (int64_t)kvh * 16 * D;
+    const KT *vbase = (const KT *)a.v + (int64_t)kvh * 16 * D;
+    const int ntiles = (key_end + kPfKeys - 1) / kPfKeys;
+
+    // ---- global -> registers -> LDS staging of one 64-key tile
+    Raw kreg[LPT], vreg[LPT];
+    float sreg = 0.f;
+    auto load_tile = [&](int kt) {
+#pragma unroll
+        for (int k = 0; k < LPT; ++k) {
+            const int u = tid + 256 * k;
+            const int b = u / (2 * D), within = u % (2 * D);
+            const int jb = 4 * kt + b;
+            if (16 * jb < key_end) {
+                const int blk = btr[jb];
+                const int slot = within / (D / 8), d8 = (within % (D / 8)) * 8;
+                kreg[k] = kv::load(kbase + (int64_t)blk * blk_stride + slot * D + d8);
+                const int d = within / 2, half = within % 2;
+                vreg[k] = kv::load(vbase + (int64_t)blk * blk_stride + d * 16 + 8 * half);
+            }
+        }
+        if constexpr (FP8) {
+            if (tid < 8) {
+                const int jb = 4 * kt + (tid & 3);
+                if (16 * jb < key_end) {
+                    const int64_t si = (int64_t)btr[jb] * a.num_kv_heads + kvh;
+                    sreg = tid < 4 ? a.k_scale[si] : a.v_scale[si];
+                }
+            }
+        }
+    };
+    auto store_tile = [&](int kt, int buf) {
+        uint16_t *kl = lds + buf * LD::STAGE;
+        uint16_t *vl = kl + LD::KSZ;
+#pragma unroll
+        for (int k = 0; k < LPT; ++k) {
+            const int u = tid + 256 * k;
+            const int b = u / (2 * D), within = u % (2 * D);
+            const int jb = 4 * kt + b;
+            const int slot = within / (D / 8), d8 = (within % (D / 8)) * 8;
+            const int d = within / 2, half = within % 2;
+            u32x4_t kw = {0u, 0u, 0u, 0u}, vw = {0u, 0u, 0u, 0u};
+            if (16 * jb < key_end) {
+                kw = __builtin_bit_cast(u32x4_t, kv::widen(kreg[k]));
+                const int valid = key_end - (16 * jb + 8 * half);  // keys of this 8-run in range
+                const uint32_t keep = valid >= 8 ? 0xFFu : (valid <= 0 ? 0u : ((1u << valid) - 1u));
+                vw = __builtin_bit_cast(u32x4_t, kv::widen(kv::mask(vreg[k], keep)));
+            }
+            *(u32x4_t *)(kl + (16 * b + slot) * LD::KROW + d8) = kw;
+            *(u32x4_t *)(vl + d * LD::VROW + 16 * b + 8 * half) = vw;
+        }
+        if constexpr (FP8) {
+            if (tid < 8) lscale[buf * 8 + tid] = sreg;
+        }
+    };
+
+    load_tile(0);
+    store_tile(0, 0);
+    __syncthreads();
+
+    const float scale = a.scale_log2;
+    const int ksel_row = 8 * (c16 >> 2) + (c16 & 3);  // + 4t + 32ch: S^T row -> key
+    for (int kt = 0; kt < ntiles; ++kt) {
+        const int buf = kt & 1;
+        if (kt + 1 < ntiles) load_tile(kt + 1);
+        const uint16_t *kl = lds + buf * LD::STAGE;
+        const uint16_t *vl = kl + LD::KSZ;
+#pragma unroll
+        for (int ch = 0; ch < 2; ++ch) {
+            f32x4_t s[2][2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                s[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+                s[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+                const uint16_t *krow = kl + (32 * ch + ksel_row + 4 * t) * LD::KROW + 8 * g4;
+#pragma unroll
+                for (int c = 0; c < NC; ++c) {
+                    const bf16x8_t kf = *(const bf16x8_t *)(krow + 32 * c);
+#pragma unroll
+                    for (int nn = 0; nn < 2; ++nn)
+                        s[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], s[t][nn], 0, 0, 0);
+                }
+            }
+            float sk = scale, sv = 1.f;
+            if constexpr (FP8) {
+                const int bi = 2 * ch + (g4 >> 1);
+                sk = scale * lscale[buf * 8 + bi];
+                sv = lscale[buf * 8 + 4 + bi];
+            }
+            const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
+            bf16x8_t pf[2];
+            float alpha[2];
+#pragma unroll
+            for (int nn = 0; nn < 2; ++nn) {
+                float p[8];
+                float mx = -INFINITY;
+#pragma unroll
+                for (int t = 0; t < 2; ++t)
+#pragma unroll
+                    for (int r = 0; r < 4; ++r) {
+                        const float v = s[t][nn][r] * sk;
+                        p[4 * t + r] = (key0 + 4 * t + r < klim[nn]) ? v : -INFINITY;
+                        mx = fmaxf(mx, p[4 * t + r]);
+                    }
+                mx = fmaxf(mx, __shfl_xor(mx, 16));
+                mx = fmaxf(mx, __shfl_xor(mx, 32));
+                const float m_new = fmaxf(m_run[nn], mx);
+                const float m_use = m_new == -INFINITY ? 0.f : m_new;
+                alpha[nn] = __builtin_amdgcn_exp2f(m_run[nn] - m_use);
+                float psum = 0.f;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                    p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
+                    psum += p[e];
+                }
+                l_run[nn] = l_run[nn] * alpha[nn] + psum;
+                m_run[nn] = m_new;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) pf[nn][e] = (__bf16)(p[e] * sv);
+            }
+            if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+#pragma unroll
+                for (int nn = 0; nn < 2; ++nn)
+#pragma unroll
+                    for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha[nn];
+            }
+            const uint16_t *vrow = vl + c16 * LD::VROW + 32 * ch + 8 * g4;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) {
+                const bf16x8_t vf = *(const bf16x8_t *)(vrow + 16 * i * LD::VROW);
+#pragma unroll
+                for (int nn = 0; nn < 2; ++nn)
+                    acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
+            }
+        }
+        if (kt + 1 < ntiles) store_tile(kt + 1, buf ^ 1);
+        __syncthreads();
+    }
+
+#pragma unroll
+    for (int nn = 0; nn < 2; ++nn) {
+        float l_tot = l_run[nn] + __shfl_xor(l_run[nn], 16);
+        l_tot += __shfl_xor(l_tot, 32);
+        if (!qok[nn]) continue;
+        const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
+        float *dst = a.out + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 4 * g4;
+#pragma unroll
+        for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i) = acc[nn][i] * inv;
+    }
+}
+
 // -------------------------------------------------------------------- merge
 
 template <int D>
@@ -444,8 +673,31 @@ hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, int head_dim, bool fp8,
-                            hipStream_t s) {
+template <int D, bool FP8>
+static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
+    static bool attr_set = false;
+    const int bytes = PfLds<D>::BYTES;
+    if (!attr_set) {
+        hipError_t e = hipFuncSetAttribute((const void *)prefill_kernel<D, FP8>,
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+        if (e != hipSuccess) return e;
+        attr_set = true;
+    }
+    const dim3 grid((unsigned)(8 * p.per_xcd)), block(256);
+    hipLaunchKernelGGL((prefill_kernel<D, FP8>), grid, block, bytes, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
+                            int head_dim, bool fp8, hipStream_t s) {
+    if (p.n_logical > 0) {
+        hipError_t e;
+        if (head_dim == 64 && !fp8) e = launch_prefill_t<64, false>(p, s);
+        else if (head_dim == 64) e = launch_prefill_t<64, true>(p, s);
+        else if (!fp8) e = launch_prefill_t<128, false>(p, s);
+        else e = launch_prefill_t<128, true>(p, s);
+        if (e != hipSuccess) return e;
+    }
     if (a.n_waves > 0) {
         const dim3 grid((unsigned)((a.n_waves + 3) / 4)), block(256);
         if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, a);

@@ -42,6 +42,23 @@ struct AttnArgs {
     float *out, *part_o, *part_lse;
 };
 
+struct PrefillArgs {
+    const PrefillDesc *pdesc;
+    int32_t n_pdesc;
+    int32_t n_logical;              // n_pdesc * num_kv_heads
+    int32_t per_xcd;                // logical tiles per XCD slot
+    int32_t group;                  // Hq / Hkv (<= 128)
+    const int32_t *klim;
+    const uint16_t *q;
+    int32_t num_q_heads, num_kv_heads;
+    const void *k, *v;
+    const float *k_scale, *v_scale;
+    const int32_t *block_tables;
+    int32_t max_blocks_per_row;
+    float scale_log2;
+    float *out;
+};
+
 struct MergeArgs {
     int64_t n_waves;                // merged rows * Hq
     int32_t num_q_heads, head_chunks, heads_per_chunk, group;
@@ -53,7 +70,7 @@ struct MergeArgs {
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
-hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, int head_dim, bool fp8,
-                            hipStream_t s);
+hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
+                            int head_dim, bool fp8, hipStream_t s);
 
 }  // namespace echo

@@ -188,23 +188,23 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     for (int32_t v : plan.merge_ent)
         if (v < 0) return ECHO_E_INVALID;  // every merged result must have all its parts
 
-    // ---- prefill rows: consecutive token slices, whole causal key range
+    // ---- prefill rows: tiles of consecutive tokens, all heads of a KV head
+    plan.pdesc.clear();
+    const int32_t bt_tok = std::max(1, kPrefillQueries / G);
+    plan.prefill_tokens_per_tile = bt_tok;
     for (int32_t r = 0; r < B; ++r) {
         if (b.kind[r] != ECHO_ROW_PREFILL) continue;
         const int32_t q = b.q_start[r + 1] - b.q_start[r];
         const int32_t c = b.seq_lens[r] - q;
-        for (int32_t i0 = 0; i0 < q; i0 += nt_max) {
-            const int32_t ntk = std::min(nt_max, q - i0);
-            WorkDesc d;
-            d.tok_off = b.q_start[r] + i0;
-            d.shape = ntk | kItemConsecutive;
-            d.bt_row = r;
-            d.key_begin = 0;
-            d.key_end = c + i0 + ntk;
-            d.part = -1;
-            d.pad0 = d.pad1 = 0;
-            plan.desc.push_back(d);
-            plan.stats.prefill_items += wpd;
+        const int32_t ntiles = (q + bt_tok - 1) / bt_tok;
+        for (int32_t k = ntiles - 1; k >= 0; --k) {  // longest key ranges first
+            PrefillDesc d;
+            d.row = r;
+            d.tok0 = b.q_start[r] + k * bt_tok;
+            d.ntok = std::min(bt_tok, q - k * bt_tok);
+            d.key_end = c + k * bt_tok + d.ntok;
+            plan.pdesc.push_back(d);
+            plan.stats.prefill_items += Hkv;
         }
     }
 
@@ -242,7 +242,9 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     L.n_merge_entries = n_ent;
     L.n_slots = n_slots;
     int64_t w = 0;
+    L.n_pdesc = (int64_t)plan.pdesc.size();
     L.off_desc = w;       w += L.n_desc * 8;
+    L.off_pdesc = w;      w += L.n_pdesc * 4;
     L.off_tok_list = w;   w += L.n_tok_list;
     L.off_klim = w;       w += L.n_tokens;
     L.off_merge_tok = w;  w += L.n_merge_rows;
@@ -261,6 +263,8 @@ void pack_plan(const Plan &plan, void *dst) {
     const PlanLayout &L = plan.layout;
     int32_t *w = static_cast<int32_t *>(dst);
     if (L.n_desc) std::memcpy(w + L.off_desc, plan.desc.data(), L.n_desc * sizeof(WorkDesc));
+    if (L.n_pdesc)
+        std::memcpy(w + L.off_pdesc, plan.pdesc.data(), L.n_pdesc * sizeof(PrefillDesc));
     if (L.n_tok_list)
         std::memcpy(w + L.off_tok_list, plan.tok_list.data(), L.n_tok_list * 4);
     if (L.n_tokens) std::memcpy(w + L.off_klim, plan.klim.data(), L.n_tokens * 4);

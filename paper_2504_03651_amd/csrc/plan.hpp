@@ -37,6 +37,18 @@ struct WorkDesc {      // 32 bytes
 };
 static_assert(sizeof(WorkDesc) == 32, "descriptor layout");
 
+// One tile of a prefill chunk: up to kPrefillQueries query vectors (ntok
+// consecutive tokens x all query heads of one KV head) for one workgroup.  On
+// the GPU it expands over the KV heads.
+constexpr int kPrefillQueries = 128;
+struct PrefillDesc {   // 16 bytes
+    int32_t row;
+    int32_t tok0;      // first token of the tile
+    int32_t ntok;      // tokens in the tile
+    int32_t key_end;   // keys visible to the last token
+};
+static_assert(sizeof(PrefillDesc) == 16, "prefill descriptor layout");
+
 // Wave w of the attention grid handles descriptor w / (Hkv * head_chunks),
 // KV head (w % (Hkv * head_chunks)) / head_chunks and head chunk
 // w % head_chunks; its partial slots start at
@@ -51,7 +63,9 @@ struct PlanLayout {
     int64_t n_merge_entries = 0;
     int64_t n_slots = 0;
     int32_t head_dim = 0;
+    int64_t n_pdesc = 0;
     int64_t off_desc = 0;       // WorkDesc[n_desc]
+    int64_t off_pdesc = 0;      // PrefillDesc[n_pdesc]
     int64_t off_tok_list = 0;   // int32[n_tok_list]
     int64_t off_klim = 0;       // int32[n_tokens]: keys visible to each token
     int64_t off_merge_tok = 0;  // int32[n_merge_rows]: the row's token
@@ -81,6 +95,8 @@ struct PlanOptions {
 // Host plan under construction (reused between calls on the same thread).
 struct Plan {
     std::vector<WorkDesc> desc, desc_sorted;
+    std::vector<PrefillDesc> pdesc;
+    int32_t prefill_tokens_per_tile = 1;
     std::vector<int32_t> tok_list, klim, merge_tok, merge_ptr, merge_ent;
     // scratch
     std::vector<int32_t> nro, rows, tail_start, seg_rows, cnt, moff, cursor, bucket;
