@@ -383,22 +383,29 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // ------------------------------------------------------------------ prefill
 //
 // One workgroup = 4 waves x 32 query vectors (consecutive tokens of one
-// prefill chunk x the query heads of one KV head).  K/V tiles of 64 keys are
-// gathered block by block into double-buffered LDS (bf16; e4m3 is widened on
-// the way in) and shared by the four waves.  Row padding of 16 bytes keeps
-// the 16-byte MFMA operand reads free of bank conflicts.
+// prefill chunk x the query heads of one KV head).  K/V tiles of 64 keys live
+// in double-buffered LDS as bf16 and are shared by the four waves:
+//   K  [64 keys][D]            16-byte chunk q of row r stored at q ^ (r & 7')
+//   V  [4 blocks][D][16 keys]  (the pool's block layout) with the two 16-byte
+//                              halves of row d swapped when bit 2 of d is set
+// where r & 7' = (r & 3) | ((r >> 3) & 1) << 2.  Both swizzles make the
+// 16-byte MFMA operand reads of 8 consecutive lanes hit 32 distinct banks.
+// bf16 pools are copied global -> LDS directly (global_load_lds_dwordx4, no
+// staging registers); e4m3 pools go through registers and are widened to bf16
+// on the way in.  Tiles of keys at or past the last token's position get
+// their V entries zeroed (0 * NaN is NaN for unwritten slots).
 
 constexpr int kPfKeys = 64;
 
 template <int D>
 struct PfLds {
-    static constexpr int KROW = D + 8;          // bf16 elements per K row
-    static constexpr int VROW = kPfKeys + 8;    // bf16 elements per V^T row
-    static constexpr int KSZ = kPfKeys * KROW;
-    static constexpr int VSZ = D * VROW;
-    static constexpr int STAGE = KSZ + VSZ;
-    static constexpr int BYTES = 2 * STAGE * 2 + 2 * 8 * 4;  // two stages + scales
+    static constexpr int KBYTES = kPfKeys * 2 * D;   // K region of a stage
+    static constexpr int VBYTES = 4 * 16 * D * 2;    // V region of a stage
+    static constexpr int STAGE = KBYTES + VBYTES;    // bytes
+    static constexpr int BYTES = 2 * STAGE + 2 * 8 * 4;
 };
+
+typedef __attribute__((address_space(3))) void lds_void_t;
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
@@ -407,8 +414,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     typedef typename kv::Raw Raw;
     typedef PfLds<D> LD;
     constexpr int NC = D / 32, NT = D / 16;
-    constexpr int LPT = D / 32;                 // 8-element loads per thread per tile (K and V each)
-    extern __shared__ __align__(16) uint16_t lds[];
+    constexpr int CHUNKS = D / 8;              // 16-byte chunks per K row
+    constexpr int NJ = D / 32;                 // 1 KiB copies per wave per region per tile
+    extern __shared__ __align__(16) uint8_t lds[];
     float *lscale = (float *)(lds + 2 * LD::STAGE);  // [2 stages][k 4 | v 4]
 
     const int P = blockIdx.x;
@@ -461,141 +469,198 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     const KT *kbase = (const KT *)a.k + (int64_t)kvh * 16 * D;
     const KT *vbase = (const KT *)a.v + (int64_t)kvh * 16 * D;
     const int ntiles = (key_end + kPfKeys - 1) / kPfKeys;
+    const int nblk = (key_end + 15) / 16;
+    // keys every query of the workgroup sees: tiles below this need no mask
+    const int kfull = key_end - ntok + 1;
 
-    // ---- global -> registers -> LDS staging of one 64-key tile
-    Raw kreg[LPT], vreg[LPT];
+    // Block ids travel one tile ahead in a VGPR (lane l holds block l & 3 of
+    // the tile); indices past the row's last block are clamped so that every
+    // load is unconditional and the loads of tile kt+1 overlap tile kt.
+    auto ids_load = [&](int kt) -> int { return btr[min(4 * kt + (lane & 3), nblk - 1)]; };
+
+    // where 1 KiB copy j of this wave lands, and what it fetches
+    auto k_src = [&](int j, int idv) -> const KT * {
+        const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in K region
+        const int r = off / (2 * D), phys = (off / 16) % CHUNKS;
+        const int q = phys ^ ((r & 3) | (((r >> 3) & 1) << 2));
+        const int blk = __builtin_amdgcn_readlane(idv, (wave * NJ + j) * 1024 / (32 * D));
+        return kbase + (int64_t)blk * blk_stride + (r & 15) * D + 8 * q;
+    };
+    auto v_src = [&](int j, int idv) -> const KT * {
+        const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in V region
+        const int within = off % (32 * D);
+        const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 2) & 1);
+        const int blk = __builtin_amdgcn_readlane(idv, (wave * NJ + j) * 1024 / (32 * D));
+        return vbase + (int64_t)blk * blk_stride + d * 16 + 8 * h;
+    };
+
+    Raw kreg[FP8 ? NJ : 1], vreg[FP8 ? NJ : 1];
     float sreg = 0.f;
-    auto load_tile = [&](int kt) {
+    auto issue_tile = [&](int kt, int idv, int buf) {
+        uint8_t *kl = lds + buf * LD::STAGE;
+        uint8_t *vl = kl + LD::KBYTES;
+        if constexpr (!FP8) {
 #pragma unroll
-        for (int k = 0; k < LPT; ++k) {
-            const int u = tid + 256 * k;
-            const int b = u / (2 * D), within = u % (2 * D);
-            const int jb = 4 * kt + b;
-            if (16 * jb < key_end) {
-                const int blk = btr[jb];
-                const int slot = within / (D / 8), d8 = (within % (D / 8)) * 8;
-                kreg[k] = kv::load(kbase + (int64_t)blk * blk_stride + slot * D + d8);
-                const int d = within / 2, half = within % 2;
-                vreg[k] = kv::load(vbase + (int64_t)blk * blk_stride + d * 16 + 8 * half);
+            for (int j = 0; j < NJ; ++j) {
+                __builtin_amdgcn_global_load_lds((const void *)k_src(j, idv),
+                                                 (lds_void_t *)(kl + (wave * NJ + j) * 1024), 16, 0, 0);
+                __builtin_amdgcn_global_load_lds((const void *)v_src(j, idv),
+                                                 (lds_void_t *)(vl + (wave * NJ + j) * 1024), 16, 0, 0);
             }
-        }
-        if constexpr (FP8) {
-            if (tid < 8) {
-                const int jb = 4 * kt + (tid & 3);
-                if (16 * jb < key_end) {
-                    const int64_t si = (int64_t)btr[jb] * a.num_kv_heads + kvh;
-                    sreg = tid < 4 ? a.k_scale[si] : a.v_scale[si];
-                }
+        } else {
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                kreg[j] = kv::load(k_src(j, idv));
+                vreg[j] = kv::load(v_src(j, idv));
+            }
+            if (tid < 8) {  // lane tid of wave 0 holds the id of block tid & 3
+                const int64_t si = (int64_t)idv * a.num_kv_heads + kvh;
+                sreg = tid < 4 ? a.k_scale[si] : a.v_scale[si];
             }
         }
     };
-    auto store_tile = [&](int kt, int buf) {
-        uint16_t *kl = lds + buf * LD::STAGE;
-        uint16_t *vl = kl + LD::KSZ;
-#pragma unroll
-        for (int k = 0; k < LPT; ++k) {
-            const int u = tid + 256 * k;
-            const int b = u / (2 * D), within = u % (2 * D);
-            const int jb = 4 * kt + b;
-            const int slot = within / (D / 8), d8 = (within % (D / 8)) * 8;
-            const int d = within / 2, half = within % 2;
-            u32x4_t kw = {0u, 0u, 0u, 0u}, vw = {0u, 0u, 0u, 0u};
-            if (16 * jb < key_end) {
-                kw = __builtin_bit_cast(u32x4_t, kv::widen(kreg[k]));
-                const int valid = key_end - (16 * jb + 8 * half);  // keys of this 8-run in range
-                const uint32_t keep = valid >= 8 ? 0xFFu : (valid <= 0 ? 0u : ((1u << valid) - 1u));
-                vw = __builtin_bit_cast(u32x4_t, kv::widen(kv::mask(vreg[k], keep)));
-            }
-            *(u32x4_t *)(kl + (16 * b + slot) * LD::KROW + d8) = kw;
-            *(u32x4_t *)(vl + d * LD::VROW + 16 * b + 8 * half) = vw;
-        }
+    // e4m3 only: widen the staged registers into LDS
+    auto store_tile = [&](int buf) {
         if constexpr (FP8) {
+            uint8_t *kl = lds + buf * LD::STAGE;
+            uint8_t *vl = kl + LD::KBYTES;
+#pragma unroll
+            for (int j = 0; j < NJ; ++j) {
+                *(u32x4_t *)(kl + (wave * NJ + j) * 1024 + 16 * lane) =
+                    __builtin_bit_cast(u32x4_t, kv::widen(kreg[j]));
+                *(u32x4_t *)(vl + (wave * NJ + j) * 1024 + 16 * lane) =
+                    __builtin_bit_cast(u32x4_t, kv::widen(vreg[j]));
+            }
             if (tid < 8) lscale[buf * 8 + tid] = sreg;
         }
     };
-
-    load_tile(0);
-    store_tile(0, 0);
-    __syncthreads();
+    // zero V of keys at or past key_end in the tile of buffer `buf`
+    auto zero_tail = [&](int kt, int buf) {
+        uint16_t *vl = (uint16_t *)(lds + buf * LD::STAGE + LD::KBYTES);
+        for (int e = tid; e < 4 * D * 2; e += 256) {       // 16-byte halves of all V rows
+            const int b = e / (2 * D), d = (e / 2) % D, ph = e & 1;
+            const int h = ph ^ ((d >> 2) & 1);
+            const int key = kPfKeys * kt + 16 * b + 8 * h;
+            uint16_t *dst = vl + (b * D + d) * 16 + 8 * ph;
+#pragma unroll
+            for (int x = 0; x < 8; ++x)
+                if (key + x >= key_end) dst[x] = 0;
+        }
+    };
 
     const float scale = a.scale_log2;
     const int ksel_row = 8 * (c16 >> 2) + (c16 & 3);  // + 4t + 32ch: S^T row -> key
-    for (int kt = 0; kt < ntiles; ++kt) {
-        const int buf = kt & 1;
-        if (kt + 1 < ntiles) load_tile(kt + 1);
-        const uint16_t *kl = lds + buf * LD::STAGE;
-        const uint16_t *vl = kl + LD::KSZ;
+
+    // one 32-key chunk of the tile in LDS buffer `buf`
+    auto chunk = [&](int buf, int kt, int ch, bool masked) {
+        const uint8_t *kl = lds + buf * LD::STAGE;
+        const uint8_t *vl = kl + LD::KBYTES;
+        f32x4_t s[2][2];
 #pragma unroll
-        for (int ch = 0; ch < 2; ++ch) {
-            f32x4_t s[2][2];
+        for (int t = 0; t < 2; ++t) {
+            s[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            s[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            const uint8_t *krow = kl + (32 * ch + ksel_row + 4 * t) * (2 * D);
 #pragma unroll
-            for (int t = 0; t < 2; ++t) {
-                s[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-                s[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-                const uint16_t *krow = kl + (32 * ch + ksel_row + 4 * t) * LD::KROW + 8 * g4;
-#pragma unroll
-                for (int c = 0; c < NC; ++c) {
-                    const bf16x8_t kf = *(const bf16x8_t *)(krow + 32 * c);
-#pragma unroll
-                    for (int nn = 0; nn < 2; ++nn)
-                        s[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], s[t][nn], 0, 0, 0);
-                }
-            }
-            float sk = scale, sv = 1.f;
-            if constexpr (FP8) {
-                const int bi = 2 * ch + (g4 >> 1);
-                sk = scale * lscale[buf * 8 + bi];
-                sv = lscale[buf * 8 + 4 + bi];
-            }
-            const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
-            bf16x8_t pf[2];
-            float alpha[2];
-#pragma unroll
-            for (int nn = 0; nn < 2; ++nn) {
-                float p[8];
-                float mx = -INFINITY;
-#pragma unroll
-                for (int t = 0; t < 2; ++t)
-#pragma unroll
-                    for (int r = 0; r < 4; ++r) {
-                        const float v = s[t][nn][r] * sk;
-                        p[4 * t + r] = (key0 + 4 * t + r < klim[nn]) ? v : -INFINITY;
-                        mx = fmaxf(mx, p[4 * t + r]);
-                    }
-                mx = fmaxf(mx, __shfl_xor(mx, 16));
-                mx = fmaxf(mx, __shfl_xor(mx, 32));
-                const float m_new = fmaxf(m_run[nn], mx);
-                const float m_use = m_new == -INFINITY ? 0.f : m_new;
-                alpha[nn] = __builtin_amdgcn_exp2f(m_run[nn] - m_use);
-                float psum = 0.f;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    p[e] = __builtin_amdgcn_exp2f(p[e] - m_use);
-                    psum += p[e];
-                }
-                l_run[nn] = l_run[nn] * alpha[nn] + psum;
-                m_run[nn] = m_new;
-#pragma unroll
-                for (int e = 0; e < 8; ++e) pf[nn][e] = (__bf16)(p[e] * sv);
-            }
-            if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+            for (int c = 0; c < NC; ++c) {
+                const bf16x8_t kf = *(const bf16x8_t *)(krow + 16 * ((4 * c + g4) ^ (c16 & 7)));
 #pragma unroll
                 for (int nn = 0; nn < 2; ++nn)
-#pragma unroll
-                    for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha[nn];
-            }
-            const uint16_t *vrow = vl + c16 * LD::VROW + 32 * ch + 8 * g4;
-#pragma unroll
-            for (int i = 0; i < NT; ++i) {
-                const bf16x8_t vf = *(const bf16x8_t *)(vrow + 16 * i * LD::VROW);
-#pragma unroll
-                for (int nn = 0; nn < 2; ++nn)
-                    acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
+                    s[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], s[t][nn], 0, 0, 0);
             }
         }
-        if (kt + 1 < ntiles) store_tile(kt + 1, buf ^ 1);
+        float sk = scale, sv = 1.f;
+        if constexpr (FP8) {
+            const int bi = 2 * ch + (g4 >> 1);
+            sk = scale * lscale[buf * 8 + bi];
+            sv = lscale[buf * 8 + 4 + bi];
+        }
+        const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
+        bf16x8_t pf[2];
+        float alpha[2];
+#pragma unroll
+        for (int nn = 0; nn < 2; ++nn) {
+            // bf16: scores stay raw until the exponent, exp2(s*sk - m*sk)
+            float p[8];
+            float mx = -INFINITY;
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    float v = s[t][nn][r];
+                    if constexpr (FP8) v *= sk;
+                    if (masked) v = (key0 + 4 * t + r < klim[nn]) ? v : -INFINITY;
+                    p[4 * t + r] = v;
+                    mx = fmaxf(mx, v);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run[nn], mx);
+            const float f = FP8 ? 1.f : sk;
+            const float m_use = m_new == -INFINITY ? 0.f : m_new * f;
+            alpha[nn] = __builtin_amdgcn_exp2f(m_run[nn] * f - m_use);
+            float psum = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(p[e], f, -m_use));
+                psum += p[e];
+            }
+            l_run[nn] = l_run[nn] * alpha[nn] + psum;
+            m_run[nn] = m_new;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) pf[nn][e] = (__bf16)(FP8 ? p[e] * sv : p[e]);
+        }
+        if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+#pragma unroll
+            for (int nn = 0; nn < 2; ++nn)
+#pragma unroll
+                for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha[nn];
+        }
+        const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + c16 * 32 +
+                              16 * ((g4 & 1) ^ ((c16 >> 2) & 1));
+#pragma unroll
+        for (int i = 0; i < NT; ++i) {
+            const bf16x8_t vf = *(const bf16x8_t *)(vrow + i * 16 * 32);
+#pragma unroll
+            for (int nn = 0; nn < 2; ++nn)
+                acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
+        }
+    };
+
+    int idv = ids_load(0);
+    int idv_next = ntiles > 1 ? ids_load(1) : idv;
+    issue_tile(0, idv, 0);
+    store_tile(0);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (ntiles == 1 && kPfKeys > key_end) {
+        zero_tail(0, 0);
         __syncthreads();
     }
+
+    auto step = [&](int kt, bool masked) {
+        const int buf = kt & 1;
+        if (kt + 1 < ntiles) {
+            idv = idv_next;
+            issue_tile(kt + 1, idv, buf ^ 1);
+            if (kt + 2 < ntiles) idv_next = ids_load(kt + 2);
+        }
+        chunk(buf, kt, 0, masked);
+        chunk(buf, kt, 1, masked);
+        if (kt + 1 < ntiles) {
+            store_tile(buf ^ 1);
+            __builtin_amdgcn_s_waitcnt(0);
+            __syncthreads();
+            if (kt + 2 == ntiles && kPfKeys * ntiles > key_end) {
+                zero_tail(kt + 1, buf ^ 1);
+                __syncthreads();
+            }
+        }
+    };
+    // tiles every query sees in full, then the diagonal tiles with the mask
+    const int nfull = min(kfull / kPfKeys, ntiles);
+    for (int kt = 0; kt < nfull; ++kt) step(kt, false);
+    for (int kt = nfull; kt < ntiles; ++kt) step(kt, true);
 
 #pragma unroll
     for (int nn = 0; nn < 2; ++nn) {
