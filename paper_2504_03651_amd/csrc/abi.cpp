@@ -397,6 +397,12 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
         return fail(ECHO_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
+    int32_t pf_blocks = 0;
+    for (const PrefillDesc &d : plan.pdesc)
+        pf_blocks = std::max(pf_blocks, (d.key_end + kBlock - 1) / kBlock);
+    if (pf_blocks > prefill_max_blocks(pool->head_dim))
+        return fail(ECHO_E_UNSUPPORTED, "prefill row of %d blocks exceeds the %d-block limit",
+                    pf_blocks, prefill_max_blocks(pool->head_dim));
     hipStream_t s = (hipStream_t)stream;
     rc = upload_plan(plan, workspace, s);
     if (rc) return rc;
@@ -456,6 +462,7 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     pf.max_blocks_per_row = batch->max_blocks_per_row;
     pf.scale_log2 = a.scale_log2;
     pf.out = out;
+    pf.max_blocks = pf_blocks;
     hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s);
     if (e != hipSuccess) return hip_fail(e, "attention launch");
     return ECHO_OK;

@@ -72,6 +72,16 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float y) {
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
+// max over lanes l, l^16, l^32, l^48 with VALU lane swaps (no LDS traffic):
+// each swap returns the lane's own value and its partner's, in some order.
+__device__ __forceinline__ float wave_max_xor16_32(float x) {
+    typedef uint32_t u2 __attribute__((ext_vector_type(2)));
+    const u2 a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    x = fmaxf(x, fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1])));
+    const u2 b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+    return fmaxf(x, fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1])));
+}
+
 // ------------------------------------------------------------------- append
 
 template <int D, bool FP8>
@@ -382,42 +392,66 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 
 // ------------------------------------------------------------------ prefill
 //
-// One workgroup = 4 waves x 32 query vectors (consecutive tokens of one
-// prefill chunk x the query heads of one KV head).  K/V tiles of 64 keys live
-// in double-buffered LDS as bf16 and are shared by the four waves:
-//   K  [64 keys][D]            16-byte chunk q of row r stored at q ^ (r & 7')
+// One workgroup = 8 waves x 32 query vectors (consecutive tokens of one
+// prefill chunk x the query heads of one KV head), one workgroup per CU.
+// K/V tiles of 64 keys live in a 3-stage LDS ring as bf16, shared by the
+// eight waves; bf16 tiles are requested two tiles ahead:
+//   K  [64 keys][D]            16-byte chunk q of row r stored at q ^ kswz(r)
 //   V  [4 blocks][D][16 keys]  (the pool's block layout) with the two 16-byte
-//                              halves of row d swapped when bit 2 of d is set
-// where r & 7' = (r & 3) | ((r >> 3) & 1) << 2.  Both swizzles make the
-// 16-byte MFMA operand reads of 8 consecutive lanes hit 32 distinct banks.
+//                              halves of row d swapped when bit 3 of d is set
+// kswz maps the key-row bits that differ between the 16 lanes of an MFMA
+// operand read onto distinct chunks, so every 16-lane read of 16 bytes per
+// lane touches all 64 LDS banks once (and 8-lane reads 32 banks once).
 // bf16 pools are copied global -> LDS directly (global_load_lds_dwordx4, no
 // staging registers); e4m3 pools go through registers and are widened to bf16
 // on the way in.  Tiles of keys at or past the last token's position get
 // their V entries zeroed (0 * NaN is NaN for unwritten slots).
 
 constexpr int kPfKeys = 64;
+constexpr int kPfLdsLimit = 160 * 1024;   // LDS of one gfx950 CU
+
+// Workgroup shape: W waves (32 query vectors each) and an S-stage LDS ring.
+#ifndef ECHO_PF_WAVES
+#define ECHO_PF_WAVES 8
+#endif
+#ifndef ECHO_PF_STAGES
+#define ECHO_PF_STAGES 3
+#endif
+constexpr int kPfWaves = ECHO_PF_WAVES;
+constexpr int kPfThreads = 64 * kPfWaves;
+constexpr int kPfStages = ECHO_PF_STAGES;
+static_assert(32 * kPfWaves == kPrefillQueries, "prefill tile size");
 
 template <int D>
 struct PfLds {
     static constexpr int KBYTES = kPfKeys * 2 * D;   // K region of a stage
     static constexpr int VBYTES = 4 * 16 * D * 2;    // V region of a stage
     static constexpr int STAGE = KBYTES + VBYTES;    // bytes
-    static constexpr int BYTES = 2 * STAGE + 2 * 8 * 4;
+    static constexpr int BYTES = kPfStages * STAGE + kPfStages * 8 * 4;  // + 4 bytes per block id
 };
+
+// s_waitcnt operand: vmcnt(n) with expcnt and lgkmcnt left free
+constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
 template <int D, bool FP8>
-__global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(PrefillArgs a) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
     typedef typename kv::Raw Raw;
     typedef PfLds<D> LD;
     constexpr int NC = D / 32, NT = D / 16;
     constexpr int CHUNKS = D / 8;              // 16-byte chunks per K row
-    constexpr int NJ = D / 32;                 // 1 KiB copies per wave per region per tile
+    constexpr int NJ = D / (8 * kPfWaves);     // 1 KiB copies per wave per region per tile
+    // chunk swizzle of K row r (see above): rows 32ch + 8(c16>>2) + 4t + (c16&3)
+    // are read by lane c16, so the swizzle is a function of c16 alone
+    auto kswz = [](int r) -> int {
+        return D == 128 ? ((r & 3) | ((r >> 1) & 0xC)) : (((r >> 1) & 1) | ((r >> 2) & 6));
+    };
     extern __shared__ __align__(16) uint8_t lds[];
-    float *lscale = (float *)(lds + 2 * LD::STAGE);  // [2 stages][k 4 | v 4]
+    float *lscale = (float *)(lds + kPfStages * LD::STAGE);  // [stage][k 4 | v 4]
+    int32_t *lids = (int32_t *)(lscale + kPfStages * 8);      // the row's block ids
 
     const int P = blockIdx.x;
     const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
@@ -473,48 +507,50 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // keys every query of the workgroup sees: tiles below this need no mask
     const int kfull = key_end - ntok + 1;
 
-    // Block ids travel one tile ahead in a VGPR (lane l holds block l & 3 of
-    // the tile); indices past the row's last block are clamped so that every
-    // load is unconditional and the loads of tile kt+1 overlap tile kt.
-    auto ids_load = [&](int kt) -> int { return btr[min(4 * kt + (lane & 3), nblk - 1)]; };
+    // The row's block ids (up to the last key of the tile) are staged in LDS
+    // once; tile block indices past the last block are clamped so that every
+    // copy is unconditional (keys past key_end are zeroed or masked instead).
+    for (int e = tid; e < nblk; e += kPfThreads) lids[e] = btr[e];
+    __syncthreads();
+    auto blk_of = [&](int kt, int b) -> int { return lids[min(4 * kt + b, nblk - 1)]; };
 
     // where 1 KiB copy j of this wave lands, and what it fetches
-    auto k_src = [&](int j, int idv) -> const KT * {
+    auto k_src = [&](int j, int kt) -> const KT * {
         const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in K region
         const int r = off / (2 * D), phys = (off / 16) % CHUNKS;
-        const int q = phys ^ ((r & 3) | (((r >> 3) & 1) << 2));
-        const int blk = __builtin_amdgcn_readlane(idv, (wave * NJ + j) * 1024 / (32 * D));
+        const int q = phys ^ kswz(r);
+        const int blk = blk_of(kt, (wave * NJ + j) * 1024 / (32 * D));
         return kbase + (int64_t)blk * blk_stride + (r & 15) * D + 8 * q;
     };
-    auto v_src = [&](int j, int idv) -> const KT * {
+    auto v_src = [&](int j, int kt) -> const KT * {
         const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in V region
         const int within = off % (32 * D);
-        const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 2) & 1);
-        const int blk = __builtin_amdgcn_readlane(idv, (wave * NJ + j) * 1024 / (32 * D));
+        const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 3) & 1);
+        const int blk = blk_of(kt, (wave * NJ + j) * 1024 / (32 * D));
         return vbase + (int64_t)blk * blk_stride + d * 16 + 8 * h;
     };
 
     Raw kreg[FP8 ? NJ : 1], vreg[FP8 ? NJ : 1];
     float sreg = 0.f;
-    auto issue_tile = [&](int kt, int idv, int buf) {
+    auto issue_tile = [&](int kt, int buf) {
         uint8_t *kl = lds + buf * LD::STAGE;
         uint8_t *vl = kl + LD::KBYTES;
         if constexpr (!FP8) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                __builtin_amdgcn_global_load_lds((const void *)k_src(j, idv),
+                __builtin_amdgcn_global_load_lds((const void *)k_src(j, kt),
                                                  (lds_void_t *)(kl + (wave * NJ + j) * 1024), 16, 0, 0);
-                __builtin_amdgcn_global_load_lds((const void *)v_src(j, idv),
+                __builtin_amdgcn_global_load_lds((const void *)v_src(j, kt),
                                                  (lds_void_t *)(vl + (wave * NJ + j) * 1024), 16, 0, 0);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                kreg[j] = kv::load(k_src(j, idv));
-                vreg[j] = kv::load(v_src(j, idv));
+                kreg[j] = kv::load(k_src(j, kt));
+                vreg[j] = kv::load(v_src(j, kt));
             }
-            if (tid < 8) {  // lane tid of wave 0 holds the id of block tid & 3
-                const int64_t si = (int64_t)idv * a.num_kv_heads + kvh;
+            if (tid < 8) {
+                const int64_t si = (int64_t)blk_of(kt, tid & 3) * a.num_kv_heads + kvh;
                 sreg = tid < 4 ? a.k_scale[si] : a.v_scale[si];
             }
         }
@@ -537,9 +573,9 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
     // zero V of keys at or past key_end in the tile of buffer `buf`
     auto zero_tail = [&](int kt, int buf) {
         uint16_t *vl = (uint16_t *)(lds + buf * LD::STAGE + LD::KBYTES);
-        for (int e = tid; e < 4 * D * 2; e += 256) {       // 16-byte halves of all V rows
+        for (int e = tid; e < 4 * D * 2; e += kPfThreads) {  // 16-byte halves of all V rows
             const int b = e / (2 * D), d = (e / 2) % D, ph = e & 1;
-            const int h = ph ^ ((d >> 2) & 1);
+            const int h = ph ^ ((d >> 3) & 1);
             const int key = kPfKeys * kt + 16 * b + 8 * h;
             uint16_t *dst = vl + (b * D + d) * 16 + 8 * ph;
 #pragma unroll
@@ -550,74 +586,87 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
 
     const float scale = a.scale_log2;
     const int ksel_row = 8 * (c16 >> 2) + (c16 & 3);  // + 4t + 32ch: S^T row -> key
+    const int kswz_lane = kswz(ksel_row);
 
-    // one 32-key chunk of the tile in LDS buffer `buf`
-    auto chunk = [&](int buf, int kt, int ch, bool masked) {
-        const uint8_t *kl = lds + buf * LD::STAGE;
-        const uint8_t *vl = kl + LD::KBYTES;
-        f32x4_t s[2][2];
+    // One 64-key tile in LDS buffer `buf`, as a two-chunk software pipeline:
+    //   QK(c0) | QK(c1) + exp(c0) | PV(c0) + exp(c1) | PV(c1)
+    // so that each run of MFMAs has independent VALU work to co-issue with.
+    // Probabilities are taken against a reference m_run (log2 units) fixed
+    // for the tile; it moves at the end of the tile when the tile's max
+    // exceeds it by more than 8 (rescaling acc and l), or, before a chunk's
+    // exponentials, when a chunk's max exceeds it by more than 64 (rare guard
+    // that also covers the first tile, where m_run is still -inf).
+    auto qk = [&](const uint8_t *kl, int ch, f32x4_t (&sc)[2][2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
-            s[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-            s[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            sc[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            sc[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
             const uint8_t *krow = kl + (32 * ch + ksel_row + 4 * t) * (2 * D);
 #pragma unroll
             for (int c = 0; c < NC; ++c) {
-                const bf16x8_t kf = *(const bf16x8_t *)(krow + 16 * ((4 * c + g4) ^ (c16 & 7)));
+                const bf16x8_t kf = *(const bf16x8_t *)(krow + 16 * ((4 * c + g4) ^ kswz_lane));
 #pragma unroll
                 for (int nn = 0; nn < 2; ++nn)
-                    s[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], s[t][nn], 0, 0, 0);
+                    sc[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], sc[t][nn], 0, 0, 0);
             }
         }
-        float sk = scale, sv = 1.f;
+    };
+    const float f = FP8 ? 1.f : scale;  // raw score -> log2 units (e4m3 scales first)
+    // scale (e4m3), mask, and the chunk max per query column in log2 units
+    auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2],
+                    float &svc) {
+        float sk = scale;
+        svc = 1.f;
         if constexpr (FP8) {
             const int bi = 2 * ch + (g4 >> 1);
             sk = scale * lscale[buf * 8 + bi];
-            sv = lscale[buf * 8 + 4 + bi];
+            svc = lscale[buf * 8 + 4 + bi];
         }
         const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
-        bf16x8_t pf[2];
-        float alpha[2];
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
-            // bf16: scores stay raw until the exponent, exp2(s*sk - m*sk)
-            float p[8];
             float mx = -INFINITY;
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    float v = s[t][nn][r];
+                    float v = sc[t][nn][r];
                     if constexpr (FP8) v *= sk;
                     if (masked) v = (key0 + 4 * t + r < klim[nn]) ? v : -INFINITY;
-                    p[4 * t + r] = v;
+                    sc[t][nn][r] = v;
                     mx = fmaxf(mx, v);
                 }
-            mx = fmaxf(mx, __shfl_xor(mx, 16));
-            mx = fmaxf(mx, __shfl_xor(mx, 32));
-            const float m_new = fmaxf(m_run[nn], mx);
-            const float f = FP8 ? 1.f : sk;
-            const float m_use = m_new == -INFINITY ? 0.f : m_new * f;
-            alpha[nn] = __builtin_amdgcn_exp2f(m_run[nn] * f - m_use);
-            float psum = 0.f;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) {
-                p[e] = __builtin_amdgcn_exp2f(__builtin_fmaf(p[e], f, -m_use));
-                psum += p[e];
-            }
-            l_run[nn] = l_run[nn] * alpha[nn] + psum;
-            m_run[nn] = m_new;
-#pragma unroll
-            for (int e = 0; e < 8; ++e) pf[nn][e] = (__bf16)(FP8 ? p[e] * sv : p[e]);
+            mc[nn] = wave_max_xor16_32(mx) * f;
         }
-        if (__any(alpha[0] != 1.f || alpha[1] != 1.f)) {
+    };
+    auto rescale = [&](const float (&mnew)[2]) {
 #pragma unroll
-            for (int nn = 0; nn < 2; ++nn)
+        for (int nn = 0; nn < 2; ++nn) {
+            const float alpha = m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mnew[nn]);
+            l_run[nn] *= alpha;
 #pragma unroll
-                for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha[nn];
+            for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha;
+            m_run[nn] = mnew[nn];
         }
+    };
+    // exponentials of one chunk against m_run, packed to bf16
+    auto expo = [&](const f32x4_t (&sc)[2][2], float svc, bf16x8_t (&pf)[2]) {
+#pragma unroll
+        for (int nn = 0; nn < 2; ++nn) {
+            const float muse = m_run[nn] == -INFINITY ? 0.f : m_run[nn];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, -muse));
+                    l_run[nn] += pe;
+                    pf[nn][4 * t + r] = (__bf16)(FP8 ? pe * svc : pe);
+                }
+        }
+    };
+    auto pv = [&](const uint8_t *vl, int ch, const bf16x8_t (&pf)[2]) {
         const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + c16 * 32 +
-                              16 * ((g4 & 1) ^ ((c16 >> 2) & 1));
+                              16 * ((g4 & 1) ^ ((c16 >> 3) & 1));
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             const bf16x8_t vf = *(const bf16x8_t *)(vrow + i * 16 * 32);
@@ -626,33 +675,81 @@ __global__ __launch_bounds__(256, 2) void prefill_kernel(PrefillArgs a) {
                 acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
         }
     };
+    auto tile = [&](int buf, int kt, bool masked) {
+        const uint8_t *kl = lds + buf * LD::STAGE;
+        const uint8_t *vl = kl + LD::KBYTES;
+        f32x4_t s0[2][2], s1[2][2];
+        float m0[2], m1[2], sv0, sv1;
+        bf16x8_t p0[2], p1[2];
+        qk(kl, 0, s0);
+        prep(buf, kt, 0, masked, s0, m0, sv0);
+        if (__any(m0[0] > m_run[0] + 64.f || m0[1] > m_run[1] + 64.f)) {
+            const float mn[2] = {fmaxf(m_run[0], m0[0]), fmaxf(m_run[1], m0[1])};
+            rescale(mn);
+        }
+        qk(kl, 1, s1);          // MFMA ...
+        expo(s0, sv0, p0);      // ... with the exponentials of chunk 0
+        prep(buf, kt, 1, masked, s1, m1, sv1);
+        if (__any(m1[0] > m_run[0] + 64.f || m1[1] > m_run[1] + 64.f)) {
+            // chunk 0's probabilities, not yet added, move with the reference
+            const float mn[2] = {fmaxf(m_run[0], m1[0]), fmaxf(m_run[1], m1[1])};
+#pragma unroll
+            for (int nn = 0; nn < 2; ++nn) {
+                const float alpha =
+                    m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mn[nn]);
+#pragma unroll
+                for (int e = 0; e < 8; ++e) p0[nn][e] = (__bf16)((float)p0[nn][e] * alpha);
+            }
+            rescale(mn);
+        }
+        pv(vl, 0, p0);          // MFMA ...
+        expo(s1, sv1, p1);      // ... with the exponentials of chunk 1
+        pv(vl, 1, p1);
+        const float mt[2] = {fmaxf(m0[0], m1[0]), fmaxf(m0[1], m1[1])};
+        if (__any(mt[0] > m_run[0] + 8.f || mt[1] > m_run[1] + 8.f)) {
+            const float mn[2] = {mt[0] > m_run[0] + 8.f ? mt[0] : m_run[0],
+                                 mt[1] > m_run[1] + 8.f ? mt[1] : m_run[1]};
+            rescale(mn);
+        }
+    };
 
-    int idv = ids_load(0);
-    int idv_next = ntiles > 1 ? ids_load(1) : idv;
-    issue_tile(0, idv, 0);
+    // Pipeline.  bf16: iteration kt loads the block ids of tile kt+3, starts
+    // the copies of tile kt+2, computes tile kt, then waits until its own
+    // copies of tile kt+1 have landed (the newer ones stay in flight) and
+    // meets the other waves at the barrier.  e4m3: tile kt+1 is staged in
+    // registers during tile kt and widened into LDS before the barrier.
+    constexpr int LA = (FP8 || kPfStages == 2) ? 1 : 2;  // tiles in flight ahead
+    const int tail_tile = (kPfKeys * ntiles > key_end) ? ntiles - 1 : -1;
+    issue_tile(0, 0);
     store_tile(0);
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (ntiles == 1 && kPfKeys > key_end) {
+    if (LA == 2 && ntiles > 1) issue_tile(1, 1);
+    if (LA == 2 && ntiles > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
+    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    __builtin_amdgcn_s_barrier();
+    if (tail_tile == 0) {
         zero_tail(0, 0);
         __syncthreads();
     }
 
     auto step = [&](int kt, bool masked) {
-        const int buf = kt & 1;
-        if (kt + 1 < ntiles) {
-            idv = idv_next;
-            issue_tile(kt + 1, idv, buf ^ 1);
-            if (kt + 2 < ntiles) idv_next = ids_load(kt + 2);
+        const int buf = kt % kPfStages;
+        bool ahead = false;   // copies of tile kt+2 issued after those of kt+1
+        if constexpr (LA == 2) {
+            if (kt + 2 < ntiles) {
+                issue_tile(kt + 2, (kt + 2) % kPfStages);
+                ahead = true;
+            }
+        } else {
+            if (kt + 1 < ntiles) issue_tile(kt + 1, (kt + 1) % kPfStages);
         }
-        chunk(buf, kt, 0, masked);
-        chunk(buf, kt, 1, masked);
+        tile(buf, kt, masked);
         if (kt + 1 < ntiles) {
-            store_tile(buf ^ 1);
-            __builtin_amdgcn_s_waitcnt(0);
-            __syncthreads();
-            if (kt + 2 == ntiles && kPfKeys * ntiles > key_end) {
-                zero_tail(kt + 1, buf ^ 1);
+            if constexpr (LA == 1) store_tile((kt + 1) % kPfStages);
+            if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
+            else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+            __builtin_amdgcn_s_barrier();
+            if (kt + 1 == tail_tile) {
+                zero_tail(kt + 1, (kt + 1) % kPfStages);
                 __syncthreads();
             }
         }
@@ -738,17 +835,21 @@ hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+int prefill_max_blocks(int head_dim) {
+    return (kPfLdsLimit - (head_dim == 64 ? PfLds<64>::BYTES : PfLds<128>::BYTES)) / 4;
+}
+
 template <int D, bool FP8>
 static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
     static bool attr_set = false;
-    const int bytes = PfLds<D>::BYTES;
+    const int bytes = PfLds<D>::BYTES + 4 * p.max_blocks;
     if (!attr_set) {
         hipError_t e = hipFuncSetAttribute((const void *)prefill_kernel<D, FP8>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, bytes);
+                                           hipFuncAttributeMaxDynamicSharedMemorySize, kPfLdsLimit);
         if (e != hipSuccess) return e;
         attr_set = true;
     }
-    const dim3 grid((unsigned)(8 * p.per_xcd)), block(256);
+    const dim3 grid((unsigned)(8 * p.per_xcd)), block(kPfThreads);
     hipLaunchKernelGGL((prefill_kernel<D, FP8>), grid, block, bytes, s, p);
     return hipGetLastError();
 }

@@ -57,6 +57,7 @@ struct PrefillArgs {
     int32_t max_blocks_per_row;
     float scale_log2;
     float *out;
+    int32_t max_blocks;             // most blocks any tile's row reads (ids staged in LDS)
 };
 
 struct MergeArgs {
@@ -70,6 +71,9 @@ struct MergeArgs {
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
+// Largest number of block ids the prefill kernel can stage for one row.
+int prefill_max_blocks(int head_dim);
+
 hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
                             int head_dim, bool fp8, hipStream_t s);
 

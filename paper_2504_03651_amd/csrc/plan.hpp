@@ -40,7 +40,10 @@ static_assert(sizeof(WorkDesc) == 32, "descriptor layout");
 // One tile of a prefill chunk: up to kPrefillQueries query vectors (ntok
 // consecutive tokens x all query heads of one KV head) for one workgroup.  On
 // the GPU it expands over the KV heads.
-constexpr int kPrefillQueries = 128;
+#ifndef ECHO_PF_WAVES
+#define ECHO_PF_WAVES 8
+#endif
+constexpr int kPrefillQueries = 32 * ECHO_PF_WAVES;
 struct PrefillDesc {   // 16 bytes
     int32_t row;
     int32_t tok0;      // first token of the tile
