@@ -141,9 +141,9 @@ int echo_block_copy(const echo_kv_pool_t *pool, const int32_t *pairs, int32_t n_
 
 /* What the planner made of a batch: a host-only call (no GPU work). */
 typedef struct {
-    int64_t work_items;         /* wave-sized attention work items */
-    int64_t decode_items;
-    int64_t prefill_items;
+    int64_t work_items;         /* decode_items + prefill_items */
+    int64_t decode_items;       /* decode waves: (key range, query slice, KV head) */
+    int64_t prefill_items;      /* prefill workgroups: (token tile, KV head) */
     int64_t shared_segments;    /* block runs read once for several decode rows */
     int64_t partial_slots;      /* split results merged after the main pass */
     int64_t merged_queries;     /* (token, head) pairs that need the merge */

@@ -360,7 +360,7 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
     int rc = plan_for(pool, batch, num_q_heads, plan);
     if (rc) return rc;
     std::memset(stats, 0, sizeof *stats);
-    stats->work_items = plan.layout.n_desc * plan.waves_per_desc;
+    stats->work_items = plan.stats.decode_items + plan.stats.prefill_items;
     stats->decode_items = plan.stats.decode_items;
     stats->prefill_items = plan.stats.prefill_items;
     stats->shared_segments = plan.stats.shared_segments;
