@@ -29,25 +29,16 @@ typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // ------------------------------------------------------------------- codecs
 
-// OCP e4m3fn byte -> exact bf16 bits (every e4m3 value is a bf16 value).
-__device__ __forceinline__ uint32_t e4m3_to_bf16_bits(uint32_t x) {
-    const uint32_t s = (x & 0x80u) << 8;
-    const uint32_t e = (x >> 3) & 15u, m = x & 7u;
-    if (e == 15u && m == 7u) return s | 0x7FC0u;
-    if (e != 0u) return s | ((e + 120u) << 7) | (m << 4);
-    // subnormal m * 2^-9: exact through fp32
-    const float f = (float)m * 0x1p-9f;
-    return s | (__float_as_uint(f) >> 16);
-}
-
+// OCP e4m3fn -> bf16, exact (every e4m3 value is a bf16 value): gfx950's
+// v_cvt_scalef32_pk_bf16_fp8 with scale 1 widens two codes per instruction
+// (checked on all 256 codes, NaN and signed zero included).
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
 __device__ __forceinline__ bf16x8_t e4m3x8_to_bf16x8(u32x2_t w) {
-    u32x4_t o;
-#pragma unroll
-    for (int k = 0; k < 4; ++k) {
-        const uint32_t word = w[k >> 1] >> (16 * (k & 1));
-        o[k] = e4m3_to_bf16_bits(word & 0xFFu) | (e4m3_to_bf16_bits((word >> 8) & 0xFFu) << 16);
-    }
-    return __builtin_bit_cast(bf16x8_t, o);
+    const bf16x2_t a = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, false);
+    const bf16x2_t b = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[0], 1.0f, true);
+    const bf16x2_t c = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, false);
+    const bf16x2_t d = __builtin_amdgcn_cvt_scalef32_pk_bf16_fp8(w[1], 1.0f, true);
+    return (bf16x8_t){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
 // fp32 -> OCP e4m3fn, round to nearest even, saturating to +-448.
