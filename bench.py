@@ -1,16 +1,22 @@
 #!/usr/bin/env python3
 """Benchmark of one mixed serving iteration over a paged KV cache on one MI355X.
 
-A step is the whole hot path on one synthetic batch: copy-on-write block
-copies, KV append, then mixed attention (decode split-KV + prefill chunks +
-merge), all through the C ABI on one stream.  Inputs are resident in HBM
-before the timed region.  Prints one JSON line.
+A step is the whole hot path on one synthetic batch, through the C ABI on one
+stream: copy-on-write block copies, KV append, then mixed attention (prefill
+chunks, decode split-KV with shared prefixes read once, merge).  Inputs are
+resident in HBM before the timed region.  Prints one JSON line.
 
     python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+
+`value` is query tokens per second of whole steps.  The roofline object is
+for the step's dominant kernel, timed with HIP events that the library
+records around each launch on the same stream (echo_profile), over K more
+steps after the timed ones.
 """
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -24,6 +30,8 @@ sys.path.insert(0, ROOT)
 METRIC = "mixed-iteration attention tokens/s; decode HBM GB/s and prefill MFMA % of peak"
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+KERNEL_SOURCE = os.path.join(ROOT, "paper_2504_03651_amd", "csrc", "kernels.hip")
 
 DESCRIPTIONS = {
     1: "tiny mixed batch: 2 decode + 2 prefill rows, MHA 4x64, 64-block pool",
@@ -45,6 +53,7 @@ def parse():
     ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
+    ap.add_argument("--copy-pairs", type=int, default=1024)
     return ap.parse_args()
 
 
@@ -52,9 +61,28 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def kernel_source_hash() -> str:
+    with open(KERNEL_SOURCE, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(config: int, kernel: str):
+    """HBM bytes per launch from the committed rocprofv3 counter runs, or None
+    when they are missing or were taken on a different kernel source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if t.get("kernels_sha256_16") != kernel_source_hash():
+        return None
+    e = t.get("entries", {}).get(f"cfg{config}:{kernel}")
+    return None if e is None else int(e["bytes_per_launch"])
+
+
 def cpu_baseline(w, threads):
-    """The fp64 oracle on the host cores: the whole iteration when it is
-    short, else a bounded sample of queries (stated in the record)."""
+    """The fp64 oracle on the host cores: the whole iteration when it fits the
+    budget, else a bounded sample of query vectors (stated in the record)."""
     import oracle
     from tests.gpu_util import compact
     c, _ = compact(w)
@@ -67,14 +95,13 @@ def cpu_baseline(w, threads):
     oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
     t_app = time.perf_counter() - t0
     T, Hq = c.batch.num_tokens, c.num_q_heads
-    # estimate the cost of all queries from their key counts, sample if long
     q = np.diff(c.batch.q_start)
     klim = np.concatenate([c.batch.seq_lens[r] - q[r] + 1 + np.arange(q[r])
                            for r in range(c.batch.num_rows)])
     budget_keys = 1.5e8 * threads    # roughly 10-20 s of fp64 work
     total_keys = float(klim.sum()) * Hq
     if total_keys <= budget_keys:
-        sel, frac, what = None, 1.0, "whole iteration (all queries)"
+        sel, frac, what = None, 1.0, "all query vectors"
     else:
         g = np.random.Generator(np.random.PCG64(0))
         n = int(T * Hq * budget_keys / total_keys)
@@ -85,17 +112,41 @@ def cpu_baseline(w, threads):
     oracle.attention(pool, c.batch, c.q, Hq, c.sm_scale, sel=sel, threads=threads)
     t_attn = time.perf_counter() - t0
     t_iter = t_app + t_attn / frac
-    return {"value": T / t_iter, "unit": "tokens/s", "cores": threads, "kind": "oracle",
-            "sample": f"append of the full batch + attention over {what}; time scaled to the "
-                      f"whole iteration ({t_app:.2f} s append, {t_attn:.2f} s attention measured; "
-                      f"pool build {t_prep:.1f} s not counted)"}
+    return {"value": round(T / t_iter, 3), "unit": "tokens/s", "cores": threads, "kind": "oracle",
+            "sample": f"copy + append of the full batch and attention over {what}, time scaled "
+                      f"to the whole iteration ({t_app:.2f} s copy+append, {t_attn:.2f} s "
+                      f"attention measured; pool build {t_prep:.1f} s not counted)"}
+
+
+def copy_benchmark(it, w, n_pairs, reps=5):
+    """R/W bandwidth of echo_block_copy on n_pairs disjoint (used -> free) pairs."""
+    import torch
+    from paper_2504_03651_amd import echo
+    g = np.random.Generator(np.random.PCG64(10))
+    n = min(n_pairs, len(w.used_blocks), len(w.free_blocks))
+    src = g.choice(w.used_blocks, size=n, replace=False)
+    dst = g.choice(w.free_blocks, size=n, replace=False)
+    pairs = np.stack([src, dst], 1).astype(np.int32)
+    dpairs = torch.from_numpy(pairs).cuda()
+    echo.block_copy(it.pool, dpairs, pairs)
+    s, e = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    s.record()
+    for _ in range(reps):
+        echo.block_copy(it.pool, dpairs, pairs)
+    e.record()
+    torch.cuda.synchronize()
+    ms = s.elapsed_time(e) / reps
+    block_bytes = w.num_kv_heads * 16 * w.head_dim * w.kv_bytes_per_elem()
+    moved = 2 * 2 * n * block_bytes          # K and V, read and write
+    return {"pairs": n, "ms": round(ms, 4), "bytes": moved, "GBps": round(moved / ms / 1e6, 1)}
 
 
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the hot path "
-              "shards by KV head or prefix group with no exchange, but this build runs on a "
+              "shards by KV head or by prefix group with no exchange, but this build runs on a "
               "single MI355X.", file=sys.stderr)
         return 2
     import torch
@@ -118,55 +169,70 @@ def main():
     torch.cuda.synchronize()
     log(f"[bench] {args.warmup} warmup steps done")
 
+    # ---- timed steps
     stream = torch.cuda.current_stream()
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(args.steps)]
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     t_host = time.perf_counter()
-    for k in range(args.steps):
-        e = ev[k]
-        e[0].record(stream)
-        it.copy()
-        e[1].record(stream)
-        it.append()
-        e[2].record(stream)
-        it.attend()
-        e[3].record(stream)
+    for _ in range(args.steps):
+        it.step()
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_host
     ms = start.elapsed_time(stop) / args.steps
-    t_copy = np.mean([e[0].elapsed_time(e[1]) for e in ev])
-    t_app = np.mean([e[1].elapsed_time(e[2]) for e in ev])
-    t_attn = np.mean([e[2].elapsed_time(e[3]) for e in ev])
-    log(f"[bench] {args.steps} steps: {ms:.3f} ms/step (copy {t_copy:.3f}, append {t_app:.3f}, "
-        f"attention {t_attn:.3f}); host wall {wall / args.steps * 1e3:.3f} ms/step")
+    log(f"[bench] {args.steps} steps: {ms:.4f} ms/step (host wall {wall / args.steps * 1e3:.4f})")
 
+    # ---- per-kernel times, HIP events recorded by the library on this stream
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    timings = []
+    echo.profile(True)
+    for k in range(args.steps):
+        ev[k][0].record(stream)
+        it.copy()
+        ev[k][1].record(stream)
+        it.append()
+        ev[k][2].record(stream)
+        it.attend()
+        timings.append(echo.attn_timing())
+    echo.profile(False)
+    torch.cuda.synchronize()
+    kms = {name: float(np.mean([t[name] for t in timings])) for name in timings[0]}
+    kms["block_copy_ms"] = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
+    kms["kv_append_ms"] = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
+    log("[bench] per-kernel ms: " + ", ".join(f"{k} {v:.4f}" for k, v in kms.items()))
+
+    # ---- roofline of the dominant kernel
     T, Hq, Hkv, D = w.batch.num_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
     eb = w.kv_bytes_per_elem()
-    tok_bytes = 2 * Hkv * D * eb + (2 * Hkv * 4 if eb == 1 else 0) / 16
-    q_out = T * Hq * D * (2 + 4)
-    kv_unique = st["unique_kv_tokens"] * tok_bytes
-    kv_logical = st["logical_kv_tokens"] * tok_bytes
-    attn_bytes = kv_unique + q_out
-    flops = 4.0 * Hq * D * st["causal_pairs"]
-    achieved_gbs = attn_bytes / (t_attn * 1e-3) / 1e9
-    achieved_tflops = flops / (t_attn * 1e-3) / 1e12
-    hbm_time = attn_bytes / (HBM_PEAK_GBS * 1e9)
-    mfma_time = flops / (BF16_PEAK_TFLOPS * 1e12)
-    if hbm_time >= mfma_time:
-        roof = {"bound": "hbm", "achieved": round(achieved_gbs, 1), "peak": HBM_PEAK_GBS,
-                "unit": "GB/s", "frac": round(achieved_gbs / HBM_PEAK_GBS, 4)}
+    kv_tok = 2 * D * eb + (2 * 4 / 16 if eb == 1 else 0)   # K+V bytes per token per KV head
+    n_dec = int((w.batch.row_kind == W.DECODE).sum())
+    dec_bytes = st["decode_kv_tokens"] * Hkv * kv_tok + n_dec * Hq * D * (2 + 4)
+    pf_flops = 4.0 * Hq * D * st["prefill_causal_pairs"]
+    if kms["decode_ms"] >= kms["prefill_ms"]:
+        t_k = kms["decode_ms"] * 1e-3
+        achieved = dec_bytes / t_k / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4),
+                "traffic": measured_traffic(args.config, "attn_kernel"),
+                "kernel": "attn_kernel (decode split-KV, shared prefixes read once)",
+                "algorithmic_bytes": int(dec_bytes), "avg_ms": round(kms["decode_ms"], 4)}
     else:
-        roof = {"bound": "mfma", "achieved": round(achieved_tflops, 1), "peak": BF16_PEAK_TFLOPS,
-                "unit": "TFLOP/s", "frac": round(achieved_tflops / BF16_PEAK_TFLOPS, 4)}
-    roof["traffic"] = None
-    roof["kernel"] = "echo_attn_mixed (plan upload + attn_items_kernel + merge_kernel)"
-    roof["algorithmic_bytes"] = int(attn_bytes)
-    roof["algorithmic_flops"] = int(flops)
-    roof["avg_ms"] = round(float(t_attn), 4)
+        t_k = kms["prefill_ms"] * 1e-3
+        achieved = pf_flops / t_k / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 1), "peak": BF16_PEAK_TFLOPS,
+                "unit": "TFLOP/s", "frac": round(achieved / BF16_PEAK_TFLOPS, 4),
+                "traffic": measured_traffic(args.config, "prefill_kernel"),
+                "kernel": "prefill_kernel (bf16 MFMA, causal chunks)",
+                "algorithmic_flops": int(pf_flops), "avg_ms": round(kms["prefill_ms"], 4)}
+    side = {}
+    if kms["decode_ms"] > 0:
+        side["decode_GBps"] = round(dec_bytes / (kms["decode_ms"] * 1e-3) / 1e9, 1)
+        side["decode_frac_hbm"] = round(side["decode_GBps"] / HBM_PEAK_GBS, 4)
+    if kms["prefill_ms"] > 0:
+        side["prefill_TFLOPs"] = round(pf_flops / (kms["prefill_ms"] * 1e-3) / 1e12, 1)
+        side["prefill_frac_mfma"] = round(side["prefill_TFLOPs"] / BF16_PEAK_TFLOPS, 4)
 
     rec = {"metric": METRIC, "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s",
            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
@@ -178,12 +244,11 @@ def main():
                       "kv_heads": Hkv, "head_dim": D, "pool_blocks": w.num_blocks,
                       "cow_pairs": int(w.cow_pairs.shape[0])},
            "roofline": roof,
-           "kernels_ms": {"block_copy": round(float(t_copy), 4), "kv_append": round(float(t_app), 4),
-                          "attention": round(float(t_attn), 4)},
-           "decode_gbs": {"unique": round(achieved_gbs, 1),
-                          "logical": round((kv_logical + q_out) / (t_attn * 1e-3) / 1e9, 1)},
-           "attention_tflops": round(achieved_tflops, 2),
+           "kernels_ms": {k: round(v, 4) for k, v in kms.items()},
+           "side_rooflines": side,
            "plan": st}
+    if args.copy_pairs > 0:
+        rec["block_copy_bench"] = copy_benchmark(it, w, args.copy_pairs)
     if not args.no_cpu_baseline:
         threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         log(f"[bench] timing the oracle on {threads} host threads")

@@ -150,6 +150,8 @@ typedef struct {
     int64_t unique_kv_tokens;   /* per KV head: distinct (block, slot) pairs read */
     int64_t logical_kv_tokens;  /* per KV head: sum over rows of seq_lens */
     int64_t causal_pairs;       /* per query head: sum over queries of visible keys */
+    int64_t decode_kv_tokens;   /* per KV head: keys the decode items read (shared runs once) */
+    int64_t prefill_causal_pairs; /* per query head: causal_pairs of the prefill rows only */
     int64_t workspace_bytes;
 } echo_plan_stats_t;
 
@@ -160,6 +162,24 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
 /* Host-only validation of pool and batch as echo_kv_append (for_append = 1)
  * or echo_attn_mixed (for_append = 0) would do it; no GPU work. */
 int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t for_append);
+
+/* Per-kernel GPU time of the calling thread's most recent echo_attn_mixed
+ * call, measured with HIP events recorded on that call's stream around the
+ * plan upload and each kernel launch.  Recording is off unless enabled with
+ * echo_profile(1) on the same thread; kernels not launched report 0. */
+typedef struct {
+    float upload_ms;    /* plan upload (host -> device copy) */
+    float prefill_ms;   /* prefill_kernel: chunked-prefill tiles */
+    float decode_ms;    /* attn_kernel: decode split-KV / shared-prefix items */
+    float merge_ms;     /* merge_kernel: log-sum-exp merge of partial results */
+} echo_attn_timing_t;
+
+/* Turns event recording on (1) or off (0) for this thread; returns the
+ * previous setting.  Recording adds a few events per call, nothing else. */
+int echo_profile(int enable);
+
+/* Waits for the last profiled call's events and fills *timing. */
+int echo_attn_timing(echo_attn_timing_t *timing);
 
 /* Static name of a status code. */
 const char *echo_status_string(int status);

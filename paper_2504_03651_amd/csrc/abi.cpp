@@ -205,6 +205,36 @@ struct Staging {
 };
 Staging g_staging[64];
 
+// Opt-in per-kernel timing (echo_profile / echo_attn_timing).
+struct Profile {
+    bool on = false;
+    bool valid = false;
+    int device = -1;
+    hipEvent_t ev[8] = {};          // upload pair, then one pair per kernel
+    bool launched[4] = {};          // upload, prefill, decode, merge
+};
+thread_local Profile g_prof;
+
+int profile_events(hipEvent_t **out) {
+    *out = nullptr;
+    if (!g_prof.on) return ECHO_OK;
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
+    if (g_prof.device != dev) {
+        for (hipEvent_t &x : g_prof.ev) {
+            if (x) (void)hipEventDestroy(x);
+            x = nullptr;
+        }
+        g_prof.device = dev;
+    }
+    for (hipEvent_t &x : g_prof.ev) {
+        if (!x && (e = hipEventCreate(&x)) != hipSuccess) return hip_fail(e, "hipEventCreate");
+    }
+    *out = g_prof.ev;
+    return ECHO_OK;
+}
+
 int upload_plan(const Plan &plan, void *workspace, hipStream_t stream) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
@@ -260,6 +290,31 @@ const char *echo_status_string(int status) {
 }
 
 const char *echo_last_error(void) { return g_error.c_str(); }
+
+int echo_profile(int enable) {
+    const int prev = g_prof.on ? 1 : 0;
+    g_prof.on = enable != 0;
+    return prev;
+}
+
+int echo_attn_timing(echo_attn_timing_t *t) {
+    g_error.clear();
+    if (!t) return fail(ECHO_E_INVALID, "timing is NULL");
+    if (!g_prof.valid) return fail(ECHO_E_INVALID, "no profiled echo_attn_mixed call on this thread");
+    float ms[4] = {0.f, 0.f, 0.f, 0.f};
+    for (int k = 0; k < 4; ++k) {
+        if (!g_prof.launched[k]) continue;
+        hipError_t e = hipEventSynchronize(g_prof.ev[2 * k + 1]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
+        e = hipEventElapsedTime(&ms[k], g_prof.ev[2 * k], g_prof.ev[2 * k + 1]);
+        if (e != hipSuccess) return hip_fail(e, "hipEventElapsedTime");
+    }
+    t->upload_ms = ms[0];
+    t->prefill_ms = ms[1];
+    t->decode_ms = ms[2];
+    t->merge_ms = ms[3];
+    return ECHO_OK;
+}
 
 int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t for_append) {
     g_error.clear();
@@ -368,6 +423,8 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
     stats->merged_queries = plan.layout.n_merge_rows * num_q_heads;
     stats->logical_kv_tokens = plan.stats.logical_kv_tokens;
     stats->causal_pairs = plan.stats.causal_pairs;
+    stats->decode_kv_tokens = plan.stats.decode_kv_tokens;
+    stats->prefill_causal_pairs = plan.stats.prefill_causal_pairs;
     stats->workspace_bytes = plan.layout.total_words * 4;
     // distinct (block, slot) pairs that the batch reads
     std::vector<uint8_t> used((size_t)pool->num_blocks, 0);
@@ -404,8 +461,20 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
         return fail(ECHO_E_UNSUPPORTED, "prefill row of %d blocks exceeds the %d-block limit",
                     pf_blocks, prefill_max_blocks(pool->head_dim));
     hipStream_t s = (hipStream_t)stream;
+    hipEvent_t *ev = nullptr;
+    rc = profile_events(&ev);
+    if (rc) return rc;
+    g_prof.valid = false;
+    if (ev) {
+        hipError_t e0 = hipEventRecord(ev[0], s);
+        if (e0 != hipSuccess) return hip_fail(e0, "hipEventRecord");
+    }
     rc = upload_plan(plan, workspace, s);
     if (rc) return rc;
+    if (ev) {
+        hipError_t e0 = hipEventRecord(ev[1], s);
+        if (e0 != hipSuccess) return hip_fail(e0, "hipEventRecord");
+    }
 
     const PlanLayout &L = plan.layout;
     int32_t *w = (int32_t *)workspace;
@@ -463,8 +532,14 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     pf.scale_log2 = a.scale_log2;
     pf.out = out;
     pf.max_blocks = pf_blocks;
-    hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s);
+    hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s,
+                                    ev ? ev + 2 : nullptr);
     if (e != hipSuccess) return hip_fail(e, "attention launch");
+    g_prof.valid = ev != nullptr;
+    g_prof.launched[0] = true;
+    g_prof.launched[1] = pf.n_logical > 0;
+    g_prof.launched[2] = a.n_waves > 0;
+    g_prof.launched[3] = m.n_waves > 0;
     return ECHO_OK;
 }
 

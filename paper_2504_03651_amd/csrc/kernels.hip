@@ -846,29 +846,36 @@ static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
 }
 
 hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
-                            int head_dim, bool fp8, hipStream_t s) {
+                            int head_dim, bool fp8, hipStream_t s, hipEvent_t *ev) {
+    hipError_t e;
+    // event pairs only around kernels that launch: an empty pair still costs
+    // GPU time between the two records
     if (p.n_logical > 0) {
-        hipError_t e;
+        if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
         if (head_dim == 64 && !fp8) e = launch_prefill_t<64, false>(p, s);
         else if (head_dim == 64) e = launch_prefill_t<64, true>(p, s);
         else if (!fp8) e = launch_prefill_t<128, false>(p, s);
         else e = launch_prefill_t<128, true>(p, s);
         if (e != hipSuccess) return e;
+        if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
     }
     if (a.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return e;
         const dim3 grid((unsigned)((a.n_waves + 3) / 4)), block(256);
         if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, a);
         else if (head_dim == 64) hipLaunchKernelGGL((attn_kernel<64, true>), grid, block, 0, s, a);
         else if (!fp8) hipLaunchKernelGGL((attn_kernel<128, false>), grid, block, 0, s, a);
         else hipLaunchKernelGGL((attn_kernel<128, true>), grid, block, 0, s, a);
-        hipError_t e = hipGetLastError();
-        if (e != hipSuccess) return e;
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return e;
     }
     if (m.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[4], s)) != hipSuccess) return e;
         const dim3 grid((unsigned)((m.n_waves + 3) / 4)), block(256);
         if (head_dim == 64) hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, s, m);
         else hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, s, m);
-        return hipGetLastError();
+        if ((e = hipGetLastError()) != hipSuccess) return e;
+        if (ev && (e = hipEventRecord(ev[5], s)) != hipSuccess) return e;
     }
     return hipSuccess;
 }

@@ -74,7 +74,10 @@ hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
 // Largest number of block ids the prefill kernel can stage for one row.
 int prefill_max_blocks(int head_dim);
 
+// Launches prefill, decode and merge kernels in that order.  With `ev` set,
+// records ev[2k] before and ev[2k+1] after kernel k (0 prefill, 1 decode,
+// 2 merge), for the kernels that launch.
 hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
-                            int head_dim, bool fp8, hipStream_t s);
+                            int head_dim, bool fp8, hipStream_t s, hipEvent_t *ev);
 
 }  // namespace echo

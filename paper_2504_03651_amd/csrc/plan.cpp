@@ -99,6 +99,8 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         for (int32_t i = 0; i < q; ++i) kl[i] = c + i + 1;
         plan.stats.logical_kv_tokens += b.seq_lens[r];
         plan.stats.causal_pairs += (int64_t)q * c + (int64_t)q * (q + 1) / 2;
+        if (b.kind[r] == ECHO_ROW_PREFILL)
+            plan.stats.prefill_causal_pairs += (int64_t)q * c + (int64_t)q * (q + 1) / 2;
     }
 
     // ---- decode rows: segments from the trie plus one private tail per row
@@ -157,6 +159,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             plan.tok_list.push_back(b.q_start[seg_rows[s.rows_off + k]]);
         const int32_t rep = seg_rows[s.rows_off];
         const bool direct = (s.nrows == 1 && cnt[rep] == 1);
+        plan.stats.decode_kv_tokens += s.key_end - kBlock * s.j0;
         for (int32_t j = s.j0; j < s.j1; j += split) {
             const int32_t jend = std::min(j + split, s.j1);
             for (int32_t k0 = 0; k0 < s.nrows; k0 += nt_max) {

@@ -83,6 +83,7 @@ struct PlanLayout {
 struct PlanStats {
     int64_t decode_items = 0, prefill_items = 0, shared_segments = 0;
     int64_t logical_kv_tokens = 0, causal_pairs = 0;
+    int64_t decode_kv_tokens = 0, prefill_causal_pairs = 0;
 };
 
 struct HostBatch {

@@ -26,7 +26,8 @@ KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
 SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes", "echo_block_copy",
-           "echo_attn_plan_stats", "echo_validate", "echo_status_string", "echo_last_error"]
+           "echo_attn_plan_stats", "echo_validate", "echo_status_string", "echo_last_error",
+           "echo_profile", "echo_attn_timing"]
 
 
 class EchoError(RuntimeError):
@@ -57,7 +58,11 @@ class CPlanStats(ctypes.Structure):
     _fields_ = [(n, ctypes.c_int64) for n in (
         "work_items", "decode_items", "prefill_items", "shared_segments", "partial_slots",
         "merged_queries", "unique_kv_tokens", "logical_kv_tokens", "causal_pairs",
-        "workspace_bytes")]
+        "decode_kv_tokens", "prefill_causal_pairs", "workspace_bytes")]
+
+
+class CAttnTiming(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_float) for n in ("upload_ms", "prefill_ms", "decode_ms", "merge_ms")]
 
 
 _lib = None
@@ -84,6 +89,10 @@ def lib():
         L.echo_status_string.restype = ctypes.c_char_p
         L.echo_last_error.argtypes = []
         L.echo_last_error.restype = ctypes.c_char_p
+        L.echo_profile.argtypes = [ctypes.c_int]
+        L.echo_profile.restype = ctypes.c_int
+        L.echo_attn_timing.argtypes = [ctypes.POINTER(CAttnTiming)]
+        L.echo_attn_timing.restype = ctypes.c_int
         for name in ("echo_kv_append", "echo_attn_mixed", "echo_block_copy",
                      "echo_attn_plan_stats", "echo_validate"):
             getattr(L, name).restype = ctypes.c_int
@@ -221,6 +230,18 @@ def plan_stats(cpool: CPool, cbatch: CBatch, num_q_heads: int) -> dict:
     _check(lib().echo_attn_plan_stats(ctypes.byref(cpool), ctypes.byref(cbatch),
                                       int(num_q_heads), ctypes.byref(st)), "echo_attn_plan_stats")
     return {name: int(getattr(st, name)) for name, _ in CPlanStats._fields_}
+
+
+def profile(enable: bool) -> bool:
+    """Turn per-kernel event timing of echo_attn_mixed on or off (this thread)."""
+    return bool(lib().echo_profile(int(enable)))
+
+
+def attn_timing() -> dict:
+    """Per-kernel milliseconds of this thread's last profiled echo_attn_mixed."""
+    t = CAttnTiming()
+    _check(lib().echo_attn_timing(ctypes.byref(t)), "echo_attn_timing")
+    return {name: float(getattr(t, name)) for name, _ in CAttnTiming._fields_}
 
 
 def validate(cpool: CPool, cbatch: CBatch, for_append: bool) -> int:
