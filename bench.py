@@ -30,7 +30,7 @@ sys.path.insert(0, ROOT)
 METRIC = "mixed-iteration attention tokens/s; decode HBM GB/s and prefill MFMA % of peak"
 HBM_PEAK_GBS = 8000.0        # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0    # MI355X dense bf16 MFMA
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic.json")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "hbm_traffic.md")
 KERNEL_SOURCE = os.path.join(ROOT, "paper_2504_03651_amd", "csrc", "kernels.hip")
 
 DESCRIPTIONS = {
@@ -71,8 +71,9 @@ def measured_traffic(config: int, kernel: str):
     when they are missing or were taken on a different kernel source."""
     try:
         with open(TRAFFIC_FILE) as f:
-            t = json.load(f)
-    except (OSError, ValueError):
+            text = f.read()
+        t = json.loads(text.split("```json", 1)[1].split("```", 1)[0])
+    except (OSError, ValueError, IndexError):
         return None
     if t.get("kernels_sha256_16") != kernel_source_hash():
         return None
