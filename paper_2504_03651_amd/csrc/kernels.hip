@@ -13,8 +13,8 @@
 //   O^T[d][query]  += V^T[d][key] * P^T[key][query]
 // so each lane ends up owning one query column and the softmax statistics of
 // that query never leave the lane's 16-lane column group.  K blocks are stored
-// [16][D] and V blocks [D][16], which makes every MFMA operand one contiguous
-// 16-byte (bf16) or 8-byte (e4m3) load straight from the pool.
+// [16][D] and V blocks [D][16], which makes every MFMA operand a contiguous
+// load straight from the pool (16 bytes, or 8 for e4m3 V).
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
@@ -184,16 +184,38 @@ __global__ __launch_bounds__(256) void block_copy_kernel(BlockCopyArgs a) {
 
 // ---------------------------------------------------------------- attention
 
+// Pool loads: streamed past the L2 (non-temporal) when no other wave reads
+// the same keys, ordinary otherwise.
+template <bool B>
+struct Flag {
+    static constexpr bool value = B;
+};
+template <bool NT, typename R>
+__device__ __forceinline__ R pool_load(const void *p) {
+    if constexpr (NT) return __builtin_nontemporal_load((const R *)p);
+    else return *(const R *)p;
+}
+
+// Per-dtype pieces of the decode kernel.  A lane's K operand for the 32-wide
+// contraction chunk c is 8 values of d; which 8 is free as long as Q uses the
+// same assignment.  bf16 takes d = 32c + 8*g4 (one 16-byte load per chunk);
+// e4m3 takes d = 64(c/2) + 16*g4 + 8(c%2), so one 16-byte load of 16 codes
+// feeds two chunks and every K load is 16 bytes wide for both dtypes.
 template <bool FP8>
 struct KV;
 template <>
 struct KV<false> {
     typedef uint16_t T;
-    typedef u32x4_t Raw;   // 8 bf16
-    static __device__ __forceinline__ Raw load(const T *p) { return *(const Raw *)p; }
-    static __device__ __forceinline__ bf16x8_t widen(Raw r) { return __builtin_bit_cast(bf16x8_t, r); }
+    typedef u32x4_t VRaw;                   // 8 keys of one V^T row
+    static constexpr int KSTEP = 32;        // elements between a lane's K loads
+    static constexpr int KLANE = 8;         // elements per 16-lane group and load
+    static __device__ __forceinline__ int q_off(int c, int g4) { return 32 * c + 8 * g4; }
+    static __device__ __forceinline__ bf16x8_t k_chunk(const u32x4_t *kr, int c) {
+        return __builtin_bit_cast(bf16x8_t, kr[c]);
+    }
+    static __device__ __forceinline__ bf16x8_t widen(VRaw r) { return __builtin_bit_cast(bf16x8_t, r); }
     // zero element e (0..7) where bit e of keep is clear
-    static __device__ __forceinline__ Raw mask(Raw r, uint32_t keep) {
+    static __device__ __forceinline__ VRaw mask(VRaw r, uint32_t keep) {
 #pragma unroll
         for (int w = 0; w < 4; ++w) {
             const uint32_t m = ((keep >> (2 * w)) & 1u ? 0x0000FFFFu : 0u) |
@@ -206,10 +228,18 @@ struct KV<false> {
 template <>
 struct KV<true> {
     typedef uint8_t T;
-    typedef u32x2_t Raw;   // 8 e4m3
-    static __device__ __forceinline__ Raw load(const T *p) { return *(const Raw *)p; }
-    static __device__ __forceinline__ bf16x8_t widen(Raw r) { return e4m3x8_to_bf16x8(r); }
-    static __device__ __forceinline__ Raw mask(Raw r, uint32_t keep) {
+    typedef u32x2_t VRaw;                   // 8 e4m3 keys of one V^T row
+    static constexpr int KSTEP = 64;
+    static constexpr int KLANE = 16;
+    static __device__ __forceinline__ int q_off(int c, int g4) {
+        return 64 * (c >> 1) + 16 * g4 + 8 * (c & 1);
+    }
+    static __device__ __forceinline__ bf16x8_t k_chunk(const u32x4_t *kr, int c) {
+        const u32x4_t w = kr[c >> 1];
+        return e4m3x8_to_bf16x8((c & 1) ? (u32x2_t){w[2], w[3]} : (u32x2_t){w[0], w[1]});
+    }
+    static __device__ __forceinline__ bf16x8_t widen(VRaw r) { return e4m3x8_to_bf16x8(r); }
+    static __device__ __forceinline__ VRaw mask(VRaw r, uint32_t keep) {
 #pragma unroll
         for (int w = 0; w < 2; ++w) {
             uint32_t m = 0;
@@ -221,17 +251,30 @@ struct KV<true> {
     }
 };
 
+// Logical workgroup of physical workgroup P.  Workgroups are dispatched to
+// the 8 XCDs round-robin (P mod 8); this order gives each XCD runs of
+// kDecXcdRun consecutive logical workgroups, so the sibling waves of a shared
+// segment (consecutive descriptors) read its blocks through one L2, while
+// the heavy-first order is still dealt evenly over the XCDs.  The grid is a
+// multiple of 8 * kDecXcdRun.
+constexpr int kDecXcdRun = 16;
+__device__ __forceinline__ int dec_logical(int P) {
+    const int q = P >> 3;
+    return ((q / kDecXcdRun) * 8 + (P & 7)) * kDecXcdRun + q % kDecXcdRun;
+}
+
 template <int D, bool FP8>
 __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
-    typedef typename kv::Raw Raw;
-    constexpr int NC = D / 32;  // 32-wide d chunks of the QK contraction
-    constexpr int NT = D / 16;  // 16-row d tiles of O^T
+    typedef typename kv::VRaw VRaw;
+    constexpr int NC = D / 32;            // 32-wide d chunks of the QK contraction
+    constexpr int NT = D / 16;            // 16-row d tiles of O^T
+    constexpr int NK = D / kv::KSTEP;     // 16-byte K loads per key row and lane
 
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t idx = (int64_t)blockIdx.x * 4 + wave;
+    const int64_t idx = (int64_t)dec_logical(blockIdx.x) * 4 + wave;
     if (idx >= a.n_waves) return;
     const int di = (int)(idx / a.waves_per_desc);
     const int rem = (int)(idx - (int64_t)di * a.waves_per_desc);
@@ -255,19 +298,19 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const bool qvalid = qi < nt;
     int tok = 0, klim = 0;
     if (qvalid) {
-        tok = (shape & kItemConsecutive) ? tok_off + qi : a.tok_list[tok_off + qi];
+        tok = a.tok_list[tok_off + qi];
         klim = a.klim[tok];
     }
     const int head = h0 + qj;
 
-    // Q^T as the B operand: column c16, k-values d = 32c + 8*g4 .. +8
+    // Q^T as the B operand: column c16, the 8 d values kv::q_off(c, g4) ..
     bf16x8_t qf[NC];
     {
-        const uint16_t *qp = a.q + ((int64_t)tok * a.num_q_heads + head) * D + 8 * g4;
+        const uint16_t *qp = a.q + ((int64_t)tok * a.num_q_heads + head) * D;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
             u32x4_t w = {0u, 0u, 0u, 0u};
-            if (qvalid) w = *(const u32x4_t *)(qp + 32 * c);
+            if (qvalid) w = *(const u32x4_t *)(qp + kv::q_off(c, g4));
             qf[c] = __builtin_bit_cast(bf16x8_t, w);
         }
     }
@@ -290,81 +333,88 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int vslot = 8 * (g4 & 1);
     const float scale = a.scale_log2;
 
-    for (int kb = key_begin; kb < key_end; kb += 32) {
-        const int jb = kb >> 4;
-        const int b0 = btr[jb];
-        const bool has1 = kb + 16 < key_end;
-        const int b1 = has1 ? btr[jb + 1] : b0;
-        const int kblk = ksel ? b1 : b0;
-        const int vblk = vsel ? b1 : b0;
+    auto sweep = [&](auto nt_flag) {
+        constexpr bool NTL = decltype(nt_flag)::value;
+        for (int kb = key_begin; kb < key_end; kb += 32) {
+            const int jb = kb >> 4;
+            const int b0 = btr[jb];
+            const bool has1 = kb + 16 < key_end;
+            const int b1 = has1 ? btr[jb + 1] : b0;
+            const int kblk = ksel ? b1 : b0;
+            const int vblk = vsel ? b1 : b0;
 
-        Raw kr[2][NC], vr[NT];
-        const KT *kp = kbase + (int64_t)kblk * blk_stride + kslot * D + 8 * g4;
+            u32x4_t kr[2][NK];
+            VRaw vr[NT];
+            const KT *kp = kbase + (int64_t)kblk * blk_stride + kslot * D + kv::KLANE * g4;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
+            for (int t = 0; t < 2; ++t)
 #pragma unroll
-            for (int c = 0; c < NC; ++c) kr[t][c] = kv::load(kp + 4 * t * D + 32 * c);
-        const KT *vp = vbase + (int64_t)vblk * blk_stride + c16 * 16 + vslot;
+                for (int p = 0; p < NK; ++p)
+                    kr[t][p] = pool_load<NTL, u32x4_t>(kp + 4 * t * D + kv::KSTEP * p);
+            const KT *vp = vbase + (int64_t)vblk * blk_stride + c16 * 16 + vslot;
 #pragma unroll
-        for (int i = 0; i < NT; ++i) vr[i] = kv::load(vp + i * 256);
+            for (int i = 0; i < NT; ++i) vr[i] = pool_load<NTL, VRaw>(vp + i * 256);
 
-        f32x4_t s[2];
+            f32x4_t s[2];
 #pragma unroll
-        for (int t = 0; t < 2; ++t) {
-            s[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
+            for (int t = 0; t < 2; ++t) {
+                s[t] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-            for (int c = 0; c < NC; ++c)
-                s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(kr[t][c]), qf[c], s[t],
-                                                               0, 0, 0);
-        }
-
-        float sk = scale, sv = 1.f;
-        if constexpr (FP8) {
-            sk = scale * a.k_scale[(int64_t)vblk * a.num_kv_heads + kvh];
-            sv = a.v_scale[(int64_t)vblk * a.num_kv_heads + kvh];
-        }
-        const int key0 = kb + 8 * g4;
-        float p[8];
-        float mx = -INFINITY;
-#pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-                const int key = key0 + 4 * t + r;
-                const float v = s[t][r] * sk;
-                p[4 * t + r] = (key < key_end && key < klim) ? v : -INFINITY;
-                mx = fmaxf(mx, p[4 * t + r]);
+                for (int c = 0; c < NC; ++c)
+                    s[t] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::k_chunk(kr[t], c), qf[c],
+                                                                   s[t], 0, 0, 0);
             }
-        mx = fmaxf(mx, __shfl_xor(mx, 16));
-        mx = fmaxf(mx, __shfl_xor(mx, 32));
-        const float m_new = fmaxf(m_run, mx);
-        const float m_use = m_new == -INFINITY ? 0.f : m_new;
-        const float alpha = exp2f(m_run - m_use);
-        float psum = 0.f;
-#pragma unroll
-        for (int e = 0; e < 8; ++e) {
-            p[e] = exp2f(p[e] - m_use);
-            psum += p[e];
-        }
-        l_run = l_run * alpha + psum;
-        m_run = m_new;
-#pragma unroll
-        for (int i = 0; i < NT; ++i) acc[i] *= alpha;
 
-        bf16x8_t pf;
+            float sk = scale, sv = 1.f;
+            if constexpr (FP8) {
+                sk = scale * a.k_scale[(int64_t)vblk * a.num_kv_heads + kvh];
+                sv = a.v_scale[(int64_t)vblk * a.num_kv_heads + kvh];
+            }
+            const int key0 = kb + 8 * g4;
+            float p[8];
+            float mx = -INFINITY;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) pf[e] = (__bf16)(p[e] * sv);
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+                for (int r = 0; r < 4; ++r) {
+                    const int key = key0 + 4 * t + r;
+                    const float v = s[t][r] * sk;
+                    p[4 * t + r] = (key < key_end && key < klim) ? v : -INFINITY;
+                    mx = fmaxf(mx, p[4 * t + r]);
+                }
+            mx = fmaxf(mx, __shfl_xor(mx, 16));
+            mx = fmaxf(mx, __shfl_xor(mx, 32));
+            const float m_new = fmaxf(m_run, mx);
+            const float m_use = m_new == -INFINITY ? 0.f : m_new;
+            const float alpha = exp2f(m_run - m_use);
+            float psum = 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+                p[e] = exp2f(p[e] - m_use);
+                psum += p[e];
+            }
+            l_run = l_run * alpha + psum;
+            m_run = m_new;
+#pragma unroll
+            for (int i = 0; i < NT; ++i) acc[i] *= alpha;
 
-        if (kb + 32 > key_end) {  // zero V columns past the end: 0 * NaN is NaN
-            const int valid = key_end - key0;
-            const uint32_t keep = valid >= 8 ? 0xFFu : (valid <= 0 ? 0u : ((1u << valid) - 1u));
+            bf16x8_t pf;
 #pragma unroll
-            for (int i = 0; i < NT; ++i) vr[i] = kv::mask(vr[i], keep);
+            for (int e = 0; e < 8; ++e) pf[e] = (__bf16)(p[e] * sv);
+
+            if (kb + 32 > key_end) {  // zero V columns past the end: 0 * NaN is NaN
+                const int valid = key_end - key0;
+                const uint32_t keep = valid >= 8 ? 0xFFu : (valid <= 0 ? 0u : ((1u << valid) - 1u));
+#pragma unroll
+                for (int i = 0; i < NT; ++i) vr[i] = kv::mask(vr[i], keep);
+            }
+#pragma unroll
+            for (int i = 0; i < NT; ++i)
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(vr[i]), pf, acc[i], 0, 0, 0);
         }
-#pragma unroll
-        for (int i = 0; i < NT; ++i)
-            acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(vr[i]), pf, acc[i], 0, 0, 0);
-    }
+    };
+    if (shape & kItemShared) sweep(Flag<false>{});
+    else sweep(Flag<true>{});
 
     float l_tot = l_run + __shfl_xor(l_run, 16);
     l_tot += __shfl_xor(l_tot, 32);
@@ -430,7 +480,7 @@ template <int D, bool FP8>
 __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(PrefillArgs a) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
-    typedef typename kv::Raw Raw;
+    typedef typename kv::VRaw Raw;   // 8 codes (16 or 8 bytes)
     typedef PfLds<D> LD;
     constexpr int NC = D / 32, NT = D / 16;
     constexpr int CHUNKS = D / 8;              // 16-byte chunks per K row
@@ -537,8 +587,8 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         } else {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                kreg[j] = kv::load(k_src(j, kt));
-                vreg[j] = kv::load(v_src(j, kt));
+                kreg[j] = pool_load<false, Raw>(k_src(j, kt));
+                vreg[j] = pool_load<false, Raw>(v_src(j, kt));
             }
             if (tid < 8) {
                 const int64_t si = (int64_t)blk_of(kt, tid & 3) * a.num_kv_heads + kvh;
@@ -861,7 +911,9 @@ hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const Prefill
     }
     if (a.n_waves > 0) {
         if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return e;
-        const dim3 grid((unsigned)((a.n_waves + 3) / 4)), block(256);
+        // a multiple of 8 XCD runs; logical workgroups past the end exit at once
+        const int64_t run = 8 * kDecXcdRun;
+        const dim3 grid((unsigned)(((a.n_waves + 3) / 4 + run - 1) / run * run)), block(256);
         if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, a);
         else if (head_dim == 64) hipLaunchKernelGGL((attn_kernel<64, true>), grid, block, 0, s, a);
         else if (!fp8) hipLaunchKernelGGL((attn_kernel<128, false>), grid, block, 0, s, a);

@@ -159,6 +159,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             plan.tok_list.push_back(b.q_start[seg_rows[s.rows_off + k]]);
         const int32_t rep = seg_rows[s.rows_off];
         const bool direct = (s.nrows == 1 && cnt[rep] == 1);
+        const bool shared = s.nrows > nt_max || nhc > 1;
         plan.stats.decode_kv_tokens += s.key_end - kBlock * s.j0;
         for (int32_t j = s.j0; j < s.j1; j += split) {
             const int32_t jend = std::min(j + split, s.j1);
@@ -166,7 +167,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
                 const int32_t ntk = std::min(nt_max, s.nrows - k0);
                 WorkDesc d;
                 d.tok_off = tok_base + k0;
-                d.shape = ntk;
+                d.shape = ntk | (shared ? kItemShared : 0);
                 d.bt_row = rep;
                 d.key_begin = kBlock * j;
                 d.key_end = std::min(kBlock * jend, s.key_end);

@@ -21,13 +21,16 @@ constexpr int kWaveQueries = 16;   // query vectors per wave (MFMA N dimension)
 constexpr int kWavesPerGroup = 4;  // waves per workgroup
 
 // flags in WorkDesc::shape
-constexpr int32_t kItemConsecutive = 1 << 16;  // tokens tok_off, tok_off+1, ...
+// The descriptor's keys are also read by other waves (sibling query slices of
+// a shared segment, or other head chunks of the same KV head): load them
+// through the L2 so the siblings hit there, instead of streaming them.
+constexpr int32_t kItemShared = 1 << 16;
 
 // One key range of one block table against one slice of query tokens.  On
 // the GPU it expands into num_kv_heads * head_chunks waves (a head chunk is
 // up to 16 query heads of one KV head), so the host never enumerates heads.
 struct WorkDesc {      // 32 bytes
-    int32_t tok_off;   // first token, or offset into the plan's token list
+    int32_t tok_off;   // offset of the slice's first token in the plan's token list
     int32_t shape;     // nt | flags: nt tokens in the slice
     int32_t bt_row;    // row whose block table supplies the block ids
     int32_t key_begin; // first key position, a multiple of 16
