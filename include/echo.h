@@ -168,7 +168,7 @@ int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t
  * plan upload and each kernel launch.  Recording is off unless enabled with
  * echo_profile(1) on the same thread; kernels not launched report 0. */
 typedef struct {
-    float upload_ms;    /* plan upload (host -> device copy) */
+    float upload_ms;    /* plan upload (a kernel copies it from pinned host memory) */
     float prefill_ms;   /* prefill_kernel: chunked-prefill tiles */
     float decode_ms;    /* attn_kernel: decode split-KV / shared-prefix items */
     float merge_ms;     /* merge_kernel: log-sum-exp merge of partial results */

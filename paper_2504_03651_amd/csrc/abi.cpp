@@ -190,10 +190,11 @@ int plan_for(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_
 }
 
 // Pinned host staging for plan uploads: a small ring per device, each slot
-// guarded by an event so that a buffer is refilled only after its previous
-// upload has completed.
+// guarded by an event so that a buffer is refilled only after the kernel
+// that copies it to the workspace has completed.
 struct StagingSlot {
     void *host = nullptr;
+    void *dev = nullptr;   // the same memory as the device sees it
     size_t cap = 0;
     hipEvent_t ev = nullptr;
     bool pending = false;
@@ -256,16 +257,19 @@ int upload_plan(const Plan &plan, void *workspace, hipStream_t stream) {
     const size_t bytes = (size_t)plan.layout.upload_words * 4;
     if (s.cap < bytes) {
         if (s.host) (void)hipHostFree(s.host);
-        s.host = nullptr;
+        s.host = s.dev = nullptr;
         s.cap = 0;
         const size_t cap = std::max<size_t>(bytes + bytes / 2, 1 << 20);
-        e = hipHostMalloc(&s.host, cap, hipHostMallocDefault);
+        // coherent: the upload kernel reads what the host wrote, uncached
+        e = hipHostMalloc(&s.host, cap, hipHostMallocMapped | hipHostMallocCoherent);
         if (e != hipSuccess) return hip_fail(e, "hipHostMalloc (plan staging)");
+        e = hipHostGetDevicePointer(&s.dev, s.host, 0);
+        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer (plan staging)");
         s.cap = cap;
     }
     pack_plan(plan, s.host);
-    e = hipMemcpyAsync(workspace, s.host, bytes, hipMemcpyHostToDevice, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipMemcpyAsync (plan upload)");
+    e = launch_plan_upload(s.dev, workspace, plan.layout.upload_words, stream);
+    if (e != hipSuccess) return hip_fail(e, "plan upload launch");
     e = hipEventRecord(s.ev, stream);
     if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
     s.pending = true;
@@ -345,8 +349,10 @@ int echo_kv_append(const echo_kv_pool_t *pool, const echo_batch_t *batch, const 
     a.num_blocks = pool->num_blocks;
     a.num_kv_heads = pool->num_kv_heads;
     a.max_blocks_per_row = batch->max_blocks_per_row;
-    a.blocks_per_row = std::min(batch->max_q_len / kBlock + 2, batch->max_blocks_per_row);
-    a.n_units = (int64_t)batch->num_rows * a.blocks_per_row * pool->num_kv_heads;
+    a.num_rows = batch->num_rows;
+    // a row of q new tokens writes at most q / 16 + 2 blocks
+    a.n_units = ((int64_t)batch->num_tokens / kBlock + 2 * (int64_t)batch->num_rows) *
+                pool->num_kv_heads;
     hipError_t e = launch_append(a, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3,
                                  (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(e, "append launch");
@@ -506,7 +512,6 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     m.head_chunks = plan.head_chunks;
     m.heads_per_chunk = plan.heads_per_chunk;
     m.group = a.group;
-    m.desc = a.desc;
     m.merge_tok = w + L.off_merge_tok;
     m.merge_ptr = w + L.off_merge_ptr;
     m.merge_ent = w + L.off_merge_ent;

@@ -16,6 +16,8 @@
 // [16][D] and V blocks [D][16], which makes every MFMA operand a contiguous
 // load straight from the pool (16 bytes, or 8 for e4m3 V).
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 #include <stdint.h>
 
 #include "kernels.hpp"
@@ -75,55 +77,142 @@ __device__ __forceinline__ float wave_max_xor16_32(float x) {
 
 // ------------------------------------------------------------------- append
 
+// One work unit = (row, written block, KV head).  Units are enumerated
+// without host help: every workgroup scans the rows' written-block counts
+// into LDS (windows of kAppWin rows), then each wave takes every n-th unit of
+// the window and finds its row by binary search over the prefix.
+constexpr int kAppWin = 4096;
+
+// exclusive prefix of cnt[0..n) in place (n <= kAppWin); returns the total
+__device__ __forceinline__ int block_scan_4096(int32_t *cnt, int n, int32_t *wsum) {
+    constexpr int PER = kAppWin / 256;
+    const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+    int loc = 0;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = t * PER + k;
+        loc += i < n ? cnt[i] : 0;
+    }
+    int inc = loc;  // inclusive scan over the wave
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(inc, off);
+        if (lane >= off) inc += y;
+    }
+    if (lane == 63) wsum[wave] = inc;
+    __syncthreads();
+    int before = 0, total = 0;
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+        before += w < wave ? wsum[w] : 0;
+        total += wsum[w];
+    }
+    int run = before + inc - loc;
+#pragma unroll
+    for (int k = 0; k < PER; ++k) {
+        const int i = t * PER + k;
+        if (i < n) {
+            const int c = cnt[i];
+            cnt[i] = run;
+            run += c;
+        }
+    }
+    __syncthreads();
+    return total;
+}
+
+// Lane (m, part) = (lane / 4, lane % 4) carries slot m's token: the quarter
+// `part` of its K and V rows (D / 4 values).  Slot m holds position 16j + m
+// and is written when m_lo <= m < m_hi.  K rows go straight to the pool;
+// V rows are transposed through the wave's LDS tile to [d][16 slots].  A V^T
+// row that is only partly written is read, merged and written back whole:
+// the unit is the only writer of its (block, head) tile.
 template <int D, bool FP8>
-__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
-    const int lane = threadIdx.x & 63;
-    const int64_t unit = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-    if (unit >= a.n_units) return;
-    const int h = (int)(unit % a.num_kv_heads);
-    const int64_t rest = unit / a.num_kv_heads;
-    const int k = (int)(rest % a.blocks_per_row);
-    const int r = (int)(rest / a.blocks_per_row);
+__device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, int h, int lane,
+                                            uint16_t *tr) {
     const int t0 = a.q_start[r];
     const int q = a.q_start[r + 1] - t0;
     const int L = a.seq_lens[r];
     const int p0 = L - q;
-    if (q <= 0 || p0 < 0) return;
-    const int j = p0 / 16 + k;
-    if (j > (L - 1) / 16 || j >= a.max_blocks_per_row) return;
+    if (j >= a.max_blocks_per_row) return;
     const int blk = a.block_tables[(int64_t)r * a.max_blocks_per_row + j];
     if (blk < 0 || blk >= a.num_blocks) return;
-    const int lo = p0 > 16 * j ? p0 : 16 * j;
-    const int hi = L < 16 * j + 16 ? L : 16 * j + 16;
-    const int64_t tile = ((int64_t)blk * a.num_kv_heads + h) * 16 * D;
-    const uint16_t *ksrc = a.k_new + ((int64_t)(t0 + lo - p0) * a.num_kv_heads + h) * D;
-    const uint16_t *vsrc = a.v_new + ((int64_t)(t0 + lo - p0) * a.num_kv_heads + h) * D;
+    const int sb = 16 * j;
+    const int m_lo = max(p0, sb) - sb, m_hi = min(L, sb + 16) - sb;   // written slots
+    const bool full = m_lo == 0 && m_hi == 16;
+    const int m = lane >> 2, part = lane & 3;
+    const bool mine = m >= m_lo && m < m_hi;
+    constexpr int QW = D / 32;        // 16-byte words per quarter row
     const int64_t tok_stride = (int64_t)a.num_kv_heads * D;
-    const int n = hi - lo;
+    const int64_t row_src = (int64_t)(t0 + sb - p0 + m) * tok_stride + (int64_t)h * D + part * (D / 4);
+    const int64_t tile = ((int64_t)blk * a.num_kv_heads + h) * 16 * D;
+
+    u32x4_t kw[QW], vw[QW];
+#pragma unroll
+    for (int w = 0; w < QW; ++w) {
+        kw[w] = vw[w] = (u32x4_t){0u, 0u, 0u, 0u};
+        if (mine) {
+            kw[w] = *(const u32x4_t *)(a.k_new + row_src + 8 * w);
+            vw[w] = *(const u32x4_t *)(a.v_new + row_src + 8 * w);
+        }
+    }
+    // stage V as [slot][D] bf16 in this wave's LDS tile, read back by d
+    if (mine) {
+#pragma unroll
+        for (int w = 0; w < QW; ++w) *(u32x4_t *)(tr + m * D + part * (D / 4) + 8 * w) = vw[w];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
+    constexpr int DPL = D / 64;       // d rows of V^T per lane
+    uint32_t col[16];                 // slot s of this lane's d rows (DPL bf16 each)
+#pragma unroll
+    for (int s2 = 0; s2 < 16; ++s2) {
+        if constexpr (DPL == 2) col[s2] = *(const uint32_t *)(tr + s2 * D + 2 * lane);
+        else col[s2] = tr[s2 * D + lane];
+    }
+    __builtin_amdgcn_fence(__ATOMIC_SEQ_CST, "wavefront");
 
     if constexpr (!FP8) {
         uint16_t *kdst = (uint16_t *)a.k + tile;
         uint16_t *vdst = (uint16_t *)a.v + tile;
-        constexpr int LPT = D / 8;      // lanes per token row (16 bytes each)
-        constexpr int TPP = 64 / LPT;   // token rows per pass
-        for (int i = lane / LPT; i < n; i += TPP) {
-            const u32x4_t w = *(const u32x4_t *)(ksrc + i * tok_stride + (lane % LPT) * 8);
-            *(u32x4_t *)(kdst + ((lo + i) & 15) * D + (lane % LPT) * 8) = w;
+        if (mine) {
+#pragma unroll
+            for (int w = 0; w < QW; ++w) *(u32x4_t *)(kdst + m * D + part * (D / 4) + 8 * w) = kw[w];
         }
-        for (int d = lane; d < D; d += 64)
-            for (int i = 0; i < n; ++i)
-                vdst[d * 16 + ((lo + i) & 15)] = vsrc[i * tok_stride + d];
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) {
+            uint16_t *row = vdst + (lane * DPL + e) * 16;
+            uint32_t pk[8];
+            if (!full) {
+                const u32x4_t o0 = *(const u32x4_t *)row, o1 = *(const u32x4_t *)(row + 8);
+                pk[0] = o0[0]; pk[1] = o0[1]; pk[2] = o0[2]; pk[3] = o0[3];
+                pk[4] = o1[0]; pk[5] = o1[1]; pk[6] = o1[2]; pk[7] = o1[3];
+            }
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                if (s2 >= m_lo && s2 < m_hi) {
+                    const uint32_t v = (col[s2] >> (16 * e)) & 0xFFFFu;
+                    const int sh = 16 * (s2 & 1);
+                    pk[s2 >> 1] = full && !(s2 & 1) ? v : ((pk[s2 >> 1] & ~(0xFFFFu << sh)) | (v << sh));
+                }
+            }
+            *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
+            *(u32x4_t *)(row + 8) = (u32x4_t){pk[4], pk[5], pk[6], pk[7]};
+        }
     } else {
         uint8_t *kdst = (uint8_t *)a.k + tile;
         uint8_t *vdst = (uint8_t *)a.v + tile;
         const int64_t si = (int64_t)blk * a.num_kv_heads + h;
         float sk, sv;
-        if (16 * j >= p0) {  // slot 0 written by this call: fresh scales
+        if (m_lo == 0) {  // slot 0 written by this call: fresh scales
             float ak = 0.f, av = 0.f;
-            for (int d = lane; d < D; d += 64)
-                for (int i = 0; i < n; ++i) {
-                    ak = fmaxf(ak, fabsf(bf16_bits_to_f32(ksrc[i * tok_stride + d])));
-                    av = fmaxf(av, fabsf(bf16_bits_to_f32(vsrc[i * tok_stride + d])));
+#pragma unroll
+            for (int w = 0; w < QW; ++w)
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    ak = fmaxf(ak, fmaxf(fabsf(bf16_bits_to_f32(kw[w][x] & 0xFFFFu)),
+                                         fabsf(bf16_bits_to_f32(kw[w][x] >> 16))));
+                    av = fmaxf(av, fmaxf(fabsf(bf16_bits_to_f32(vw[w][x] & 0xFFFFu)),
+                                         fabsf(bf16_bits_to_f32(vw[w][x] >> 16))));
                 }
 #pragma unroll
             for (int off = 32; off >= 1; off >>= 1) {
@@ -140,14 +229,82 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
             sk = a.k_scale[si];
             sv = a.v_scale[si];
         }
-        for (int d = lane; d < D; d += 64)
-            for (int i = 0; i < n; ++i) {
-                const int slot = (lo + i) & 15;
-                kdst[slot * D + d] =
-                    (uint8_t)f32_to_e4m3(bf16_bits_to_f32(ksrc[i * tok_stride + d]) / sk);
-                vdst[d * 16 + slot] =
-                    (uint8_t)f32_to_e4m3(bf16_bits_to_f32(vsrc[i * tok_stride + d]) / sv);
+        if (mine) {
+            // 8 codes per 16-byte bf16 word
+#pragma unroll
+            for (int w = 0; w < QW; ++w) {
+                uint32_t c[2] = {0u, 0u};
+#pragma unroll
+                for (int x = 0; x < 4; ++x) {
+                    const uint32_t lo8 = f32_to_e4m3(bf16_bits_to_f32(kw[w][x] & 0xFFFFu) / sk);
+                    const uint32_t hi8 = f32_to_e4m3(bf16_bits_to_f32(kw[w][x] >> 16) / sk);
+                    c[x >> 1] |= (lo8 | (hi8 << 8)) << (16 * (x & 1));
+                }
+                *(u32x2_t *)(kdst + m * D + part * (D / 4) + 8 * w) = (u32x2_t){c[0], c[1]};
             }
+        }
+#pragma unroll
+        for (int e = 0; e < DPL; ++e) {
+            uint8_t *row = vdst + (lane * DPL + e) * 16;
+            uint32_t pk[4] = {0u, 0u, 0u, 0u};
+            if (!full) {
+                const u32x4_t o = *(const u32x4_t *)row;
+                pk[0] = o[0]; pk[1] = o[1]; pk[2] = o[2]; pk[3] = o[3];
+            }
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                if (s2 >= m_lo && s2 < m_hi) {
+                    const uint32_t c = f32_to_e4m3(bf16_bits_to_f32((col[s2] >> (16 * e)) & 0xFFFFu) / sv);
+                    const int sh = 8 * (s2 & 3);
+                    pk[s2 >> 2] = (pk[s2 >> 2] & ~(0xFFu << sh)) | (c << sh);
+                }
+            }
+            *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
+        }
+    }
+}
+
+template <int D, bool FP8>
+__global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
+    __shared__ int32_t pre[kAppWin];
+    __shared__ int32_t wsum[4];
+    __shared__ __attribute__((aligned(16))) uint16_t vstage[4][16 * D];
+    const int lane = threadIdx.x & 63;
+    const int64_t gw = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    const int64_t nw = (int64_t)gridDim.x * 4;
+    const int H = a.num_kv_heads;
+    int64_t done = 0;  // units of earlier windows
+    for (int r0 = 0; r0 < a.num_rows; r0 += kAppWin) {
+        const int nr = min(kAppWin, a.num_rows - r0);
+        for (int i = threadIdx.x; i < nr; i += 256) {
+            const int r = r0 + i;
+            const int q = a.q_start[r + 1] - a.q_start[r];
+            const int L = a.seq_lens[r];
+            const int p0 = L - q;
+            const int jlast = min((L - 1) / 16, a.max_blocks_per_row - 1);
+            pre[i] = (q > 0 && p0 >= 0 && jlast >= p0 / 16) ? jlast - p0 / 16 + 1 : 0;
+        }
+        __syncthreads();
+        const int nblk = block_scan_4096(pre, nr, wsum);
+        const int64_t units = (int64_t)nblk * H;
+        // this wave's units of the window: global indices done + u = gw (mod nw)
+        int64_t u = (gw - done) % nw;
+        if (u < 0) u += nw;
+        for (; u < units; u += nw) {
+            const int bu = (int)(u / H);
+            const int h = (int)(u - (int64_t)bu * H);
+            int lo = 0, hi = nr - 1;  // last row i with pre[i] <= bu
+            while (lo < hi) {
+                const int mid = (lo + hi + 1) >> 1;
+                if (pre[mid] <= bu) lo = mid;
+                else hi = mid - 1;
+            }
+            const int r = r0 + lo;
+            const int p0 = a.seq_lens[r] - (a.q_start[r + 1] - a.q_start[r]);
+            append_unit<D, FP8>(a, r, p0 / 16 + (bu - pre[lo]), h, lane, vstage[threadIdx.x >> 6]);
+        }
+        done += units;
+        __syncthreads();  // pre is rewritten by the next window
     }
 }
 
@@ -398,9 +555,19 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 #pragma unroll
             for (int i = 0; i < NT; ++i) acc[i] *= alpha;
 
-            bf16x8_t pf;
+            // e4m3: p times the V scale as a bf16 pair hi + lo (two MFMAs), so
+            // that the scale is not rounded to bf16 along with every term
+            bf16x8_t pf, pl;
 #pragma unroll
-            for (int e = 0; e < 8; ++e) pf[e] = (__bf16)(p[e] * sv);
+            for (int e = 0; e < 8; ++e) {
+                if constexpr (FP8) {
+                    const float x = p[e] * sv;
+                    pf[e] = (__bf16)x;
+                    pl[e] = (__bf16)(x - (float)pf[e]);
+                } else {
+                    pf[e] = (__bf16)p[e];
+                }
+            }
 
             if (kb + 32 > key_end) {  // zero V columns past the end: 0 * NaN is NaN
                 const int valid = key_end - key0;
@@ -409,8 +576,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
                 for (int i = 0; i < NT; ++i) vr[i] = kv::mask(vr[i], keep);
             }
 #pragma unroll
-            for (int i = 0; i < NT; ++i)
-                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kv::widen(vr[i]), pf, acc[i], 0, 0, 0);
+            for (int i = 0; i < NT; ++i) {
+                const bf16x8_t vf = kv::widen(vr[i]);
+                acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf, acc[i], 0, 0, 0);
+                if constexpr (FP8) acc[i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl, acc[i], 0, 0, 0);
+            }
         }
     };
     if (shape & kItemShared) sweep(Flag<false>{});
@@ -690,8 +860,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
             m_run[nn] = mnew[nn];
         }
     };
-    // exponentials of one chunk against m_run, packed to bf16
-    auto expo = [&](const f32x4_t (&sc)[2][2], float svc, bf16x8_t (&pf)[2]) {
+    // exponentials of one chunk against m_run, packed to bf16.  e4m3: the
+    // probability times the block's V scale is carried as a bf16 pair hi + lo
+    // (P.V takes two MFMAs): one bf16 would round every term of the block
+    // by the same relative amount, up to 2^-9 of the output.
+    auto expo = [&](const f32x4_t (&sc)[2][2], float svc, bf16x8_t (&pf)[2], bf16x8_t (&pl)[2]) {
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
             const float muse = m_run[nn] == -INFINITY ? 0.f : m_run[nn];
@@ -701,19 +874,29 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                 for (int r = 0; r < 4; ++r) {
                     const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, -muse));
                     l_run[nn] += pe;
-                    pf[nn][4 * t + r] = (__bf16)(FP8 ? pe * svc : pe);
+                    if constexpr (FP8) {
+                        const float x = pe * svc;
+                        const __bf16 hb = (__bf16)x;
+                        pf[nn][4 * t + r] = hb;
+                        pl[nn][4 * t + r] = (__bf16)(x - (float)hb);
+                    } else {
+                        pf[nn][4 * t + r] = (__bf16)pe;
+                    }
                 }
         }
     };
-    auto pv = [&](const uint8_t *vl, int ch, const bf16x8_t (&pf)[2]) {
+    auto pv = [&](const uint8_t *vl, int ch, const bf16x8_t (&pf)[2], const bf16x8_t (&pl)[2]) {
         const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + c16 * 32 +
                               16 * ((g4 & 1) ^ ((c16 >> 3) & 1));
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             const bf16x8_t vf = *(const bf16x8_t *)(vrow + i * 16 * 32);
 #pragma unroll
-            for (int nn = 0; nn < 2; ++nn)
+            for (int nn = 0; nn < 2; ++nn) {
                 acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
+                if constexpr (FP8)
+                    acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[nn], acc[nn][i], 0, 0, 0);
+            }
         }
     };
     auto tile = [&](int buf, int kt, bool masked) {
@@ -721,7 +904,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         const uint8_t *vl = kl + LD::KBYTES;
         f32x4_t s0[2][2], s1[2][2];
         float m0[2], m1[2], sv0, sv1;
-        bf16x8_t p0[2], p1[2];
+        bf16x8_t p0[2], p1[2], l0[2], l1[2];
         qk(kl, 0, s0);
         prep(buf, kt, 0, masked, s0, m0, sv0);
         if (__any(m0[0] > m_run[0] + 64.f || m0[1] > m_run[1] + 64.f)) {
@@ -729,7 +912,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
             rescale(mn);
         }
         qk(kl, 1, s1);          // MFMA ...
-        expo(s0, sv0, p0);      // ... with the exponentials of chunk 0
+        expo(s0, sv0, p0, l0);  // ... with the exponentials of chunk 0
         prep(buf, kt, 1, masked, s1, m1, sv1);
         if (__any(m1[0] > m_run[0] + 64.f || m1[1] > m_run[1] + 64.f)) {
             // chunk 0's probabilities, not yet added, move with the reference
@@ -739,13 +922,22 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                 const float alpha =
                     m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mn[nn]);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) p0[nn][e] = (__bf16)((float)p0[nn][e] * alpha);
+                for (int e = 0; e < 8; ++e) {
+                    if constexpr (FP8) {
+                        const float x = ((float)p0[nn][e] + (float)l0[nn][e]) * alpha;
+                        const __bf16 hb = (__bf16)x;
+                        p0[nn][e] = hb;
+                        l0[nn][e] = (__bf16)(x - (float)hb);
+                    } else {
+                        p0[nn][e] = (__bf16)((float)p0[nn][e] * alpha);
+                    }
+                }
             }
             rescale(mn);
         }
-        pv(vl, 0, p0);          // MFMA ...
-        expo(s1, sv1, p1);      // ... with the exponentials of chunk 1
-        pv(vl, 1, p1);
+        pv(vl, 0, p0, l0);      // MFMA ...
+        expo(s1, sv1, p1, l1);  // ... with the exponentials of chunk 1
+        pv(vl, 1, p1, l1);
         const float mt[2] = {fmaxf(m0[0], m1[0]), fmaxf(m0[1], m1[1])};
         if (__any(mt[0] > m_run[0] + 8.f || mt[1] > m_run[1] + 8.f)) {
             const float mn[2] = {mt[0] > m_run[0] + 8.f ? mt[0] : m_run[0],
@@ -829,43 +1021,95 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const int jh = h - kvh * a.group - hc * 16;
     const int nh = min(a.heads_per_chunk, a.group - hc * 16);
     const int rem = kvh * a.head_chunks + hc;
-    float mx = -INFINITY;
-    for (int e = e0; e < e1; ++e) {
-        const WorkDesc *d = a.desc + a.merge_ent[2 * e];
-        const int slot = d->part + rem * (d->shape & 0xFF) * a.heads_per_chunk +
-                         a.merge_ent[2 * e + 1] * nh + jh;
-        mx = fmaxf(mx, a.part_lse[slot]);
-    }
     constexpr int PER = D / 64;
     float acc[PER];
 #pragma unroll
     for (int k = 0; k < PER; ++k) acc[k] = 0.f;
-    float wsum = 0.f;
-    for (int e = e0; e < e1; ++e) {
-        const WorkDesc *d = a.desc + a.merge_ent[2 * e];
-        const int slot = d->part + rem * (d->shape & 0xFF) * a.heads_per_chunk +
-                         a.merge_ent[2 * e + 1] * nh + jh;
-        const float lse = a.part_lse[slot];
-        const float w = lse == -INFINITY ? 0.f : exp2f(lse - mx);
-        wsum += w;
+    float mx = -INFINITY, wsum = 0.f;
+    // entries 64 at a time, one per lane: slot and lse in parallel, then the
+    // partial rows in a loop whose loads do not depend on each other
+    for (int eb = e0; eb < e1; eb += 64) {
+        const int e = eb + lane;
+        int slot = 0;
+        float lse = -INFINITY;
+        if (e < e1) {
+            const int part = a.merge_ent[2 * e], sh = a.merge_ent[2 * e + 1];
+            slot = part + rem * (sh & 0xFF) * a.heads_per_chunk + (sh >> 8) * nh + jh;
+            lse = a.part_lse[slot];
+        }
+        float bm = lse;
 #pragma unroll
-        for (int k = 0; k < PER; ++k) acc[k] += w * a.part_o[(int64_t)slot * D + lane * PER + k];
+        for (int off = 32; off >= 1; off >>= 1) bm = fmaxf(bm, __shfl_xor(bm, off));
+        const float m_new = fmaxf(mx, bm);
+        if (m_new == -INFINITY) continue;
+        const float alpha = exp2f(mx - m_new);   // 0 on the first batch
+        wsum *= alpha;
+#pragma unroll
+        for (int k = 0; k < PER; ++k) acc[k] *= alpha;
+        mx = m_new;
+        const float w = lse == -INFINITY ? 0.f : exp2f(lse - mx);
+        float ws = w;
+#pragma unroll
+        for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
+        wsum += ws;
+        const int n = min(64, e1 - eb);
+#pragma unroll 4
+        for (int i = 0; i < n; ++i) {
+            const int si = __builtin_amdgcn_readlane(slot, i);
+            const float wi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
+            const float *po = a.part_o + (int64_t)si * D + lane * PER;
+            if constexpr (PER == 2) {
+                const float2 v = *(const float2 *)po;
+                acc[0] += wi * v.x;
+                acc[1] += wi * v.y;
+            } else {
+                acc[0] += wi * po[0];
+            }
+        }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
     float *o = a.out + ((int64_t)tok * a.num_q_heads + h) * D + lane * PER;
-#pragma unroll
-    for (int k = 0; k < PER; ++k) o[k] = acc[k] * inv;
+    if constexpr (PER == 2) {
+        *(float2 *)o = make_float2(acc[0] * inv, acc[1] * inv);
+    } else {
+        o[0] = acc[0] * inv;
+    }
+}
+
+// ------------------------------------------------------------- plan upload
+//
+// Copies the packed plan from pinned, coherent host memory into the
+// workspace.  A kernel on the stream avoids the copy engine's hand-off with
+// the kernels around it; each thread moves 16 bytes per step.
+__global__ __launch_bounds__(256) void plan_upload_kernel(const uint32_t *__restrict__ src,
+                                                          uint32_t *__restrict__ dst, int64_t words) {
+    const int64_t n16 = words / 4;
+    const int64_t stride = (int64_t)gridDim.x * 256;
+    for (int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x; i < n16; i += stride)
+        ((u32x4_t *)dst)[i] = ((const u32x4_t *)src)[i];
+    const int64_t t = 4 * n16 + (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (blockIdx.x == 0 && t < words) dst[t] = src[t];
 }
 
 // ------------------------------------------------------------------ launchers
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s) {
     if (a.n_units == 0) return hipSuccess;
-    const dim3 grid((unsigned)((a.n_units + 3) / 4)), block(256);
+    // waves loop over units; a few per wave are enough to fill the chip
+    const int64_t wg = std::min<int64_t>((a.n_units + 3) / 4, 1024);
+    const dim3 grid((unsigned)wg), block(256);
     if (head_dim == 64 && !fp8) hipLaunchKernelGGL((append_kernel<64, false>), grid, block, 0, s, a);
     else if (head_dim == 64) hipLaunchKernelGGL((append_kernel<64, true>), grid, block, 0, s, a);
     else if (!fp8) hipLaunchKernelGGL((append_kernel<128, false>), grid, block, 0, s, a);
     else hipLaunchKernelGGL((append_kernel<128, true>), grid, block, 0, s, a);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan_upload(const void *src, void *dst, int64_t words, hipStream_t s) {
+    if (words == 0) return hipSuccess;
+    const int64_t wg = std::min<int64_t>((words / 4 + 255) / 256 + 1, 256);
+    hipLaunchKernelGGL(plan_upload_kernel, dim3((unsigned)wg), dim3(256), 0, s,
+                       (const uint32_t *)src, (uint32_t *)dst, words);
     return hipGetLastError();
 }
 

@@ -12,9 +12,8 @@ struct AppendArgs {
     float *k_scale, *v_scale;
     const uint16_t *k_new, *v_new;  // [T][Hkv][D] bf16 bits
     const int32_t *block_tables, *seq_lens, *q_start;
-    int32_t num_blocks, num_kv_heads, max_blocks_per_row;
-    int32_t blocks_per_row;         // written blocks per row, upper bound
-    int64_t n_units;                // rows * blocks_per_row * num_kv_heads
+    int32_t num_rows, num_blocks, num_kv_heads, max_blocks_per_row;
+    int64_t n_units;                // upper bound of (row, written block, head) units
 };
 
 struct BlockCopyArgs {
@@ -63,14 +62,16 @@ struct PrefillArgs {
 struct MergeArgs {
     int64_t n_waves;                // merged rows * Hq
     int32_t num_q_heads, head_chunks, heads_per_chunk, group;
-    const WorkDesc *desc;
-    const int32_t *merge_tok, *merge_ptr, *merge_ent;
+    const int32_t *merge_tok, *merge_ptr;
+    const int32_t *merge_ent;       // per entry: first slot of its descriptor, nt | i << 8
     const float *part_o, *part_lse;
     float *out;
 };
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
+// Copies `words` 32-bit words from device-visible pinned host memory to dst.
+hipError_t launch_plan_upload(const void *src, void *dst, int64_t words, hipStream_t s);
 // Largest number of block ids the prefill kernel can stage for one row.
 int prefill_max_blocks(int head_dim);
 

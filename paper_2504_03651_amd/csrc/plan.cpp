@@ -136,7 +136,9 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     for (const Segment &s : segs)
         for (int32_t k = 0; k < s.nrows; ++k) cnt[seg_rows[s.rows_off + k]] += n_splits(s);
 
-    // merge lists: rows with more than one contribution; entries (desc, i)
+    // merge lists: rows with more than one contribution; entries
+    // (first partial slot of the descriptor, nt | i << 8) for query i of a
+    // slice of nt tokens
     moff.assign((size_t)B, -1);
     int64_t n_ent = 0;
     for (int32_t r : R) {
@@ -175,12 +177,11 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
                 d.pad0 = d.pad1 = 0;
                 if (!direct) {
                     d.part = (int32_t)n_slots;
-                    const int32_t di = (int32_t)plan.desc.size();
                     for (int32_t i = 0; i < ntk; ++i) {
                         const int32_t m = moff[seg_rows[s.rows_off + k0 + i]];
                         const int64_t e = plan.merge_ptr[m] + cursor[m]++;
-                        plan.merge_ent[2 * e] = di;
-                        plan.merge_ent[2 * e + 1] = i;
+                        plan.merge_ent[2 * e] = d.part;
+                        plan.merge_ent[2 * e + 1] = ntk | (i << 8);
                     }
                     n_slots += wpd * ntk * hpc;
                 }
@@ -223,17 +224,11 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         };
         for (const WorkDesc &d : plan.desc) ++count[bucket(d) + 1];
         for (int32_t i = 0; i < nb; ++i) count[i + 1] += count[i];
-        // merge entries name descriptors by index: remap them after sorting
-        std::vector<int32_t> &where = plan.cursor;
-        where.resize(plan.desc.size());
+        // (merge entries name partial slots, which do not move with the order)
         plan.desc_sorted.resize(plan.desc.size());
-        for (size_t i = 0; i < plan.desc.size(); ++i) {
-            const int32_t pos = count[bucket(plan.desc[i])]++;
-            plan.desc_sorted[pos] = plan.desc[i];
-            where[i] = pos;
-        }
+        for (size_t i = 0; i < plan.desc.size(); ++i)
+            plan.desc_sorted[count[bucket(plan.desc[i])]++] = plan.desc[i];
         plan.desc.swap(plan.desc_sorted);
-        for (int64_t e = 0; e < n_ent; ++e) plan.merge_ent[2 * e] = where[plan.merge_ent[2 * e]];
     }
 
     PlanLayout &L = plan.layout;

@@ -76,7 +76,7 @@ struct PlanLayout {
     int64_t off_klim = 0;       // int32[n_tokens]: keys visible to each token
     int64_t off_merge_tok = 0;  // int32[n_merge_rows]: the row's token
     int64_t off_merge_ptr = 0;  // int32[n_merge_rows + 1]
-    int64_t off_merge_ent = 0;  // int32[2 * n_merge_entries]: (descriptor, index in slice)
+    int64_t off_merge_ent = 0;  // int32[2 * n_merge_entries]: (first slot, nt | i << 8)
     int64_t upload_words = 0;   // everything above is uploaded
     int64_t off_part_lse = 0;   // float[n_slots]
     int64_t off_part_o = 0;     // float[n_slots][head_dim]

@@ -85,6 +85,14 @@ def test_edge_rows(torch_cuda):
     _check_small(w, torch_cuda, "edge-rows")
 
 
+@pytest.mark.parametrize("kv", [W.KV_BF16, W.KV_FP8])
+def test_many_rows(torch_cuda, kv):
+    # more rows than the append kernel scans per LDS window (4096)
+    w = W.random_case(114, num_rows=4500, num_q_heads=4, num_kv_heads=2, head_dim=64,
+                      kv_dtype=kv, max_ctx=60, max_q=20, n_groups=3)
+    _check_small(w, torch_cuda, f"many-rows-{kv}")
+
+
 def test_deterministic(torch_cuda):
     w = W.random_case(110, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
                       max_ctx=2000, max_q=64)
