@@ -158,7 +158,7 @@ PlanOptions plan_options() {
     static const int split = [] {
         const char *e = getenv("ECHO_SPLIT_BLOCKS");
         int v = e ? atoi(e) : 0;
-        return v > 0 ? v : 32;
+        return v > 0 ? v : 48;
     }();
     o.split_blocks = split;
     return o;

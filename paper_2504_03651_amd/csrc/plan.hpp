@@ -96,7 +96,7 @@ struct HostBatch {
 };
 
 struct PlanOptions {
-    int split_blocks = 32;  // key blocks per decode split
+    int split_blocks = 48;  // key blocks per decode split
 };
 
 // Host plan under construction (reused between calls on the same thread).
