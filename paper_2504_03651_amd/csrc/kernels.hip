@@ -70,9 +70,9 @@ __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as
 __device__ __forceinline__ float wave_max_xor16_32(float x) {
     typedef uint32_t u2 __attribute__((ext_vector_type(2)));
     const u2 a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    x = fmaxf(x, fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1])));
+    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
     const u2 b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(x, fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1])));
+    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 // ------------------------------------------------------------------- append
@@ -708,6 +708,14 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
         for (int i = 0; i < NT; ++i) acc[nn][i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    // bf16: the softmax denominator is a P.V product with V = 1 (every row of
+    // lacc[nn] holds the column sum), so it sums exactly the rounded weights
+    // that P.V uses and costs one MFMA per chunk instead of 16 adds per lane.
+    // e4m3 carries p * scale into P.V, so it sums p on the VALU (l_run).
+    f32x4_t lacc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+    bf16x8_t ones;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
 
     const int32_t *btr = a.block_tables + (int64_t)row * a.max_blocks_per_row;
     const int64_t blk_stride = (int64_t)a.num_kv_heads * 16 * D;
@@ -725,40 +733,45 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     __syncthreads();
     auto blk_of = [&](int kt, int b) -> int { return lids[min(4 * kt + b, nblk - 1)]; };
 
-    // where 1 KiB copy j of this wave lands, and what it fetches
-    auto k_src = [&](int j, int kt) -> const KT * {
-        const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in K region
-        const int r = off / (2 * D), phys = (off / 16) % CHUNKS;
-        const int q = phys ^ kswz(r);
-        const int blk = blk_of(kt, (wave * NJ + j) * 1024 / (32 * D));
-        return kbase + (int64_t)blk * blk_stride + (r & 15) * D + 8 * q;
-    };
-    auto v_src = [&](int j, int kt) -> const KT * {
-        const int off = (wave * NJ + j) * 1024 + 16 * lane;       // byte offset in V region
+    // This wave's NJ copies of a tile all fall in block `bsel` of the tile's
+    // four; per lane, where each 16-byte piece comes from inside the block is
+    // the same for every tile, so only the block id (read from LDS once per
+    // tile, a step ahead, and made scalar) changes.
+    static_assert((32 * D) % (NJ * 1024) == 0, "a wave's copies stay inside one block");
+    const int bsel = wave * NJ * 1024 / (32 * D);
+    int k_off[NJ], v_off[NJ];
+#pragma unroll
+    for (int j = 0; j < NJ; ++j) {
+        const int off = (wave * NJ + j) * 1024 + 16 * lane;   // byte offset in the K / V region
+        const int r = off / (2 * D), q = ((off / 16) % CHUNKS) ^ kswz(r);
+        k_off[j] = (r & 15) * D + 8 * q;
         const int within = off % (32 * D);
         const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 3) & 1);
-        const int blk = blk_of(kt, (wave * NJ + j) * 1024 / (32 * D));
-        return vbase + (int64_t)blk * blk_stride + d * 16 + 8 * h;
-    };
+        v_off[j] = d * 16 + 8 * h;
+    }
+    auto tile_id = [&](int kt) -> int { return lids[min(4 * kt + bsel, nblk - 1)]; };
 
     Raw kreg[FP8 ? NJ : 1], vreg[FP8 ? NJ : 1];
     float sreg = 0.f;
-    auto issue_tile = [&](int kt, int buf) {
+    auto issue_tile = [&](int kt, int buf, int id) {
         uint8_t *kl = lds + buf * LD::STAGE;
         uint8_t *vl = kl + LD::KBYTES;
+        const int blk = __builtin_amdgcn_readfirstlane(id);
+        const KT *kb = kbase + (int64_t)blk * blk_stride;
+        const KT *vb = vbase + (int64_t)blk * blk_stride;
         if constexpr (!FP8) {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                __builtin_amdgcn_global_load_lds((const void *)k_src(j, kt),
+                __builtin_amdgcn_global_load_lds((const void *)(kb + k_off[j]),
                                                  (lds_void_t *)(kl + (wave * NJ + j) * 1024), 16, 0, 0);
-                __builtin_amdgcn_global_load_lds((const void *)v_src(j, kt),
+                __builtin_amdgcn_global_load_lds((const void *)(vb + v_off[j]),
                                                  (lds_void_t *)(vl + (wave * NJ + j) * 1024), 16, 0, 0);
             }
         } else {
 #pragma unroll
             for (int j = 0; j < NJ; ++j) {
-                kreg[j] = pool_load<false, Raw>(k_src(j, kt));
-                vreg[j] = pool_load<false, Raw>(v_src(j, kt));
+                kreg[j] = pool_load<false, Raw>(kb + k_off[j]);
+                vreg[j] = pool_load<false, Raw>(vb + v_off[j]);
             }
             if (tid < 8) {
                 const int64_t si = (int64_t)blk_of(kt, tid & 3) * a.num_kv_heads + kvh;
@@ -854,7 +867,8 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
             const float alpha = m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mnew[nn]);
-            l_run[nn] *= alpha;
+            if constexpr (FP8) l_run[nn] *= alpha;
+            else lacc[nn] *= alpha;
 #pragma unroll
             for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha;
             m_run[nn] = mnew[nn];
@@ -873,8 +887,8 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, -muse));
-                    l_run[nn] += pe;
                     if constexpr (FP8) {
+                        l_run[nn] += pe;
                         const float x = pe * svc;
                         const __bf16 hb = (__bf16)x;
                         pf[nn][4 * t + r] = hb;
@@ -897,6 +911,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                 if constexpr (FP8)
                     acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[nn], acc[nn][i], 0, 0, 0);
             }
+        }
+        if constexpr (!FP8) {
+#pragma unroll
+            for (int nn = 0; nn < 2; ++nn)
+                lacc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[nn], lacc[nn], 0, 0, 0);
         }
     };
     auto tile = [&](int buf, int kt, bool masked) {
@@ -953,9 +972,10 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // registers during tile kt and widened into LDS before the barrier.
     constexpr int LA = (FP8 || kPfStages == 2) ? 1 : 2;  // tiles in flight ahead
     const int tail_tile = (kPfKeys * ntiles > key_end) ? ntiles - 1 : -1;
-    issue_tile(0, 0);
+    issue_tile(0, 0, tile_id(0));
     store_tile(0);
-    if (LA == 2 && ntiles > 1) issue_tile(1, 1);
+    if (LA == 2 && ntiles > 1) issue_tile(1, 1, tile_id(1));
+    int id_ahead = tile_id(LA);   // block id of the next tile to issue
     if (LA == 2 && ntiles > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __builtin_amdgcn_s_barrier();
@@ -967,14 +987,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     auto step = [&](int kt, bool masked) {
         const int buf = kt % kPfStages;
         bool ahead = false;   // copies of tile kt+2 issued after those of kt+1
-        if constexpr (LA == 2) {
-            if (kt + 2 < ntiles) {
-                issue_tile(kt + 2, (kt + 2) % kPfStages);
-                ahead = true;
-            }
-        } else {
-            if (kt + 1 < ntiles) issue_tile(kt + 1, (kt + 1) % kPfStages);
+        if (kt + LA < ntiles) {
+            issue_tile(kt + LA, (kt + LA) % kPfStages, id_ahead);
+            ahead = LA == 2;
         }
+        id_ahead = tile_id(kt + LA + 1);
         tile(buf, kt, masked);
         if (kt + 1 < ntiles) {
             if constexpr (LA == 1) store_tile((kt + 1) % kPfStages);
@@ -994,8 +1011,13 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 
 #pragma unroll
     for (int nn = 0; nn < 2; ++nn) {
-        float l_tot = l_run[nn] + __shfl_xor(l_run[nn], 16);
-        l_tot += __shfl_xor(l_tot, 32);
+        float l_tot;
+        if constexpr (FP8) {
+            l_tot = l_run[nn] + __shfl_xor(l_run[nn], 16);
+            l_tot += __shfl_xor(l_tot, 32);
+        } else {
+            l_tot = lacc[nn][0];
+        }
         if (!qok[nn]) continue;
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
         float *dst = a.out + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 4 * g4;
