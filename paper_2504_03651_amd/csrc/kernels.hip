@@ -1075,18 +1075,39 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
         for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
         wsum += ws;
         const int n = min(64, e1 - eb);
-#pragma unroll 4
-        for (int i = 0; i < n; ++i) {
+        // four partial rows per step, their loads independent of each other
+        auto row = [&](int i, float (&v)[PER]) {
             const int si = __builtin_amdgcn_readlane(slot, i);
-            const float wi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
             const float *po = a.part_o + (int64_t)si * D + lane * PER;
             if constexpr (PER == 2) {
-                const float2 v = *(const float2 *)po;
-                acc[0] += wi * v.x;
-                acc[1] += wi * v.y;
+                const float2 x = *(const float2 *)po;
+                v[0] = x.x;
+                v[1] = x.y;
             } else {
-                acc[0] += wi * po[0];
+                v[0] = po[0];
             }
+        };
+        auto add = [&](int i, const float (&v)[PER]) {
+            const float wi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
+#pragma unroll
+            for (int k = 0; k < PER; ++k) acc[k] += wi * v[k];
+        };
+        int i = 0;
+        for (; i + 4 <= n; i += 4) {
+            float v0[PER], v1[PER], v2[PER], v3[PER];
+            row(i, v0);
+            row(i + 1, v1);
+            row(i + 2, v2);
+            row(i + 3, v3);
+            add(i, v0);
+            add(i + 1, v1);
+            add(i + 2, v2);
+            add(i + 3, v3);
+        }
+        for (; i < n; ++i) {
+            float v0[PER];
+            row(i, v0);
+            add(i, v0);
         }
     }
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
