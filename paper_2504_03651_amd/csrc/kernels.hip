@@ -81,10 +81,10 @@ __device__ __forceinline__ float wave_max_xor16_32(float x) {
 // without host help: every workgroup scans the rows' written-block counts
 // into LDS (windows of kAppWin rows), then each wave takes every n-th unit of
 // the window and finds its row by binary search over the prefix.
-constexpr int kAppWin = 4096;
+constexpr int kAppWin = 2048;
 
 // exclusive prefix of cnt[0..n) in place (n <= kAppWin); returns the total
-__device__ __forceinline__ int block_scan_4096(int32_t *cnt, int n, int32_t *wsum) {
+__device__ __forceinline__ int block_scan_window(int32_t *cnt, int n, int32_t *wsum) {
     constexpr int PER = kAppWin / 256;
     const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
     int loc = 0;
@@ -124,16 +124,11 @@ __device__ __forceinline__ int block_scan_4096(int32_t *cnt, int n, int32_t *wsu
 // Lane (m, part) = (lane / 4, lane % 4) carries slot m's token: the quarter
 // `part` of its K and V rows (D / 4 values).  Slot m holds position 16j + m
 // and is written when m_lo <= m < m_hi.  K rows go straight to the pool;
-// V rows are transposed through the wave's LDS tile to [d][16 slots].  A V^T
-// row that is only partly written is read, merged and written back whole:
-// the unit is the only writer of its (block, head) tile.
+// V rows are transposed through the wave's LDS tile to [d][16 slots] and
+// written as whole 16-slot rows when the block is full, else slot by slot.
 template <int D, bool FP8>
 __device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, int h, int lane,
-                                            uint16_t *tr) {
-    const int t0 = a.q_start[r];
-    const int q = a.q_start[r + 1] - t0;
-    const int L = a.seq_lens[r];
-    const int p0 = L - q;
+                                            uint16_t *tr, int t0, int p0, int L) {
     if (j >= a.max_blocks_per_row) return;
     const int blk = a.block_tables[(int64_t)r * a.max_blocks_per_row + j];
     if (blk < 0 || blk >= a.num_blocks) return;
@@ -181,22 +176,20 @@ __device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, i
 #pragma unroll
         for (int e = 0; e < DPL; ++e) {
             uint16_t *row = vdst + (lane * DPL + e) * 16;
-            uint32_t pk[8];
-            if (!full) {
-                const u32x4_t o0 = *(const u32x4_t *)row, o1 = *(const u32x4_t *)(row + 8);
-                pk[0] = o0[0]; pk[1] = o0[1]; pk[2] = o0[2]; pk[3] = o0[3];
-                pk[4] = o1[0]; pk[5] = o1[1]; pk[6] = o1[2]; pk[7] = o1[3];
-            }
+            if (full) {
+                uint32_t pk[8];
 #pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2) {
-                if (s2 >= m_lo && s2 < m_hi) {
-                    const uint32_t v = (col[s2] >> (16 * e)) & 0xFFFFu;
-                    const int sh = 16 * (s2 & 1);
-                    pk[s2 >> 1] = full && !(s2 & 1) ? v : ((pk[s2 >> 1] & ~(0xFFFFu << sh)) | (v << sh));
-                }
+                for (int m2 = 0; m2 < 8; ++m2)
+                    pk[m2] = ((col[2 * m2] >> (16 * e)) & 0xFFFFu) |
+                             (((col[2 * m2 + 1] >> (16 * e)) & 0xFFFFu) << 16);
+                *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
+                *(u32x4_t *)(row + 8) = (u32x4_t){pk[4], pk[5], pk[6], pk[7]};
+            } else {
+                // the written slots only: 2-byte stores at fixed offsets from the row
+#pragma unroll
+                for (int s2 = 0; s2 < 16; ++s2)
+                    if (s2 >= m_lo && s2 < m_hi) row[s2] = (uint16_t)(col[s2] >> (16 * e));
             }
-            *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
-            *(u32x4_t *)(row + 8) = (u32x4_t){pk[4], pk[5], pk[6], pk[7]};
         }
     } else {
         uint8_t *kdst = (uint8_t *)a.k + tile;
@@ -246,27 +239,32 @@ __device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, i
 #pragma unroll
         for (int e = 0; e < DPL; ++e) {
             uint8_t *row = vdst + (lane * DPL + e) * 16;
-            uint32_t pk[4] = {0u, 0u, 0u, 0u};
-            if (!full) {
-                const u32x4_t o = *(const u32x4_t *)row;
-                pk[0] = o[0]; pk[1] = o[1]; pk[2] = o[2]; pk[3] = o[3];
-            }
+            uint32_t code[16];
 #pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2) {
-                if (s2 >= m_lo && s2 < m_hi) {
-                    const uint32_t c = f32_to_e4m3(bf16_bits_to_f32((col[s2] >> (16 * e)) & 0xFFFFu) / sv);
-                    const int sh = 8 * (s2 & 3);
-                    pk[s2 >> 2] = (pk[s2 >> 2] & ~(0xFFu << sh)) | (c << sh);
-                }
+            for (int s2 = 0; s2 < 16; ++s2)
+                code[s2] = (s2 >= m_lo && s2 < m_hi)
+                               ? f32_to_e4m3(bf16_bits_to_f32((col[s2] >> (16 * e)) & 0xFFFFu) / sv)
+                               : 0u;
+            if (full) {
+                uint32_t pk[4];
+#pragma unroll
+                for (int m2 = 0; m2 < 4; ++m2)
+                    pk[m2] = code[4 * m2] | (code[4 * m2 + 1] << 8) | (code[4 * m2 + 2] << 16) |
+                             (code[4 * m2 + 3] << 24);
+                *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
+            } else {
+#pragma unroll
+                for (int s2 = 0; s2 < 16; ++s2)
+                    if (s2 >= m_lo && s2 < m_hi) row[s2] = (uint8_t)code[s2];
             }
-            *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
         }
     }
 }
 
 template <int D, bool FP8>
 __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
-    __shared__ int32_t pre[kAppWin];
+    __shared__ int32_t pre[kAppWin];                  // exclusive prefix of written blocks
+    __shared__ int32_t rt0[kAppWin], rp0[kAppWin], rL[kAppWin];   // first token, start, length
     __shared__ int32_t wsum[4];
     __shared__ __attribute__((aligned(16))) uint16_t vstage[4][16 * D];
     const int lane = threadIdx.x & 63;
@@ -283,9 +281,12 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
             const int p0 = L - q;
             const int jlast = min((L - 1) / 16, a.max_blocks_per_row - 1);
             pre[i] = (q > 0 && p0 >= 0 && jlast >= p0 / 16) ? jlast - p0 / 16 + 1 : 0;
+            rt0[i] = a.q_start[r];
+            rp0[i] = p0;
+            rL[i] = L;
         }
         __syncthreads();
-        const int nblk = block_scan_4096(pre, nr, wsum);
+        const int nblk = block_scan_window(pre, nr, wsum);
         const int64_t units = (int64_t)nblk * H;
         // this wave's units of the window: global indices done + u = gw (mod nw)
         int64_t u = (gw - done) % nw;
@@ -299,12 +300,95 @@ __global__ __launch_bounds__(256) void append_kernel(AppendArgs a) {
                 if (pre[mid] <= bu) lo = mid;
                 else hi = mid - 1;
             }
-            const int r = r0 + lo;
-            const int p0 = a.seq_lens[r] - (a.q_start[r + 1] - a.q_start[r]);
-            append_unit<D, FP8>(a, r, p0 / 16 + (bu - pre[lo]), h, lane, vstage[threadIdx.x >> 6]);
+            const int p0 = rp0[lo];
+            append_unit<D, FP8>(a, r0 + lo, p0 / 16 + (bu - pre[lo]), h, lane, vstage[threadIdx.x >> 6],
+                                rt0[lo], p0, rL[lo]);
         }
         done += units;
         __syncthreads();  // pre is rewritten by the next window
+    }
+}
+
+// Direct form for batches whose rows write few blocks each (decode-heavy):
+// one wave per (row, k-th written block, KV head) of a padded grid, no scan,
+// no LDS, so many waves stay resident.  Same results as append_kernel.
+template <int D, bool FP8>
+__global__ __launch_bounds__(256) void append_rows_kernel(AppendArgs a) {
+    const int lane = threadIdx.x & 63;
+    const int64_t unit = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
+    if (unit >= a.n_units) return;
+    const int H = a.num_kv_heads;
+    const int h = (int)(unit % H);
+    const int64_t rest = unit / H;
+    const int k = (int)(rest % a.blocks_per_row);
+    const int r = (int)(rest / a.blocks_per_row);
+    const int t0 = a.q_start[r];
+    const int q = a.q_start[r + 1] - t0;
+    const int L = a.seq_lens[r];
+    const int p0 = L - q;
+    if (q <= 0 || p0 < 0) return;
+    const int j = p0 / 16 + k;
+    if (j > (L - 1) / 16 || j >= a.max_blocks_per_row) return;
+    const int blk = a.block_tables[(int64_t)r * a.max_blocks_per_row + j];
+    if (blk < 0 || blk >= a.num_blocks) return;
+    const int lo = max(p0, 16 * j), n = min(L, 16 * j + 16) - lo;   // tokens written
+    const int64_t tok_stride = (int64_t)H * D;
+    const int64_t src = (int64_t)(t0 + lo - p0) * tok_stride + (int64_t)h * D;
+    const int64_t tile = ((int64_t)blk * H + h) * 16 * D;
+    constexpr int LPT = D / 8, TPP = 64 / LPT;   // K: lanes of 16 bytes per row, rows per pass
+    constexpr int DPL = D / 64;                  // V: d values per lane
+    const int kr = lane / LPT, kc = (lane % LPT) * 8;
+    if constexpr (!FP8) {
+        uint16_t *kdst = (uint16_t *)a.k + tile;
+        uint16_t *vdst = (uint16_t *)a.v + tile;
+        for (int i = kr; i < n; i += TPP)
+            *(u32x4_t *)(kdst + ((lo + i) & 15) * D + kc) =
+                *(const u32x4_t *)(a.k_new + src + i * tok_stride + kc);
+        for (int i = 0; i < n; ++i) {
+            const uint16_t *vp = a.v_new + src + i * tok_stride + lane * DPL;
+            const uint32_t w = DPL == 2 ? *(const uint32_t *)vp : (uint32_t)*vp;
+            const int slot = (lo + i) & 15;
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) vdst[(lane * DPL + e) * 16 + slot] = (uint16_t)(w >> (16 * e));
+        }
+    } else {
+        uint8_t *kdst = (uint8_t *)a.k + tile;
+        uint8_t *vdst = (uint8_t *)a.v + tile;
+        const int64_t si = (int64_t)blk * H + h;
+        float sk, sv;
+        if (16 * j >= p0) {  // slot 0 written by this call: fresh scales
+            float ak = 0.f, av = 0.f;
+            for (int i = 0; i < n; ++i)
+#pragma unroll
+                for (int e = 0; e < DPL; ++e) {
+                    const int d = lane * DPL + e;
+                    ak = fmaxf(ak, fabsf(bf16_bits_to_f32(a.k_new[src + i * tok_stride + d])));
+                    av = fmaxf(av, fabsf(bf16_bits_to_f32(a.v_new[src + i * tok_stride + d])));
+                }
+#pragma unroll
+            for (int off = 32; off >= 1; off >>= 1) {
+                ak = fmaxf(ak, __shfl_xor(ak, off));
+                av = fmaxf(av, __shfl_xor(av, off));
+            }
+            sk = ak == 0.f ? 1.f : ak / 448.0f;
+            sv = av == 0.f ? 1.f : av / 448.0f;
+            if (lane == 0) {
+                a.k_scale[si] = sk;
+                a.v_scale[si] = sv;
+            }
+        } else {
+            sk = a.k_scale[si];
+            sv = a.v_scale[si];
+        }
+        for (int i = 0; i < n; ++i) {
+            const int slot = (lo + i) & 15;
+#pragma unroll
+            for (int e = 0; e < DPL; ++e) {
+                const int d = lane * DPL + e;
+                kdst[slot * D + d] = (uint8_t)f32_to_e4m3(bf16_bits_to_f32(a.k_new[src + i * tok_stride + d]) / sk);
+                vdst[d * 16 + slot] = (uint8_t)f32_to_e4m3(bf16_bits_to_f32(a.v_new[src + i * tok_stride + d]) / sv);
+            }
+        }
     }
 }
 
@@ -1138,9 +1222,23 @@ __global__ __launch_bounds__(256) void plan_upload_kernel(const uint32_t *__rest
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s) {
     if (a.n_units == 0) return hipSuccess;
-    // waves loop over units; a few per wave are enough to fill the chip
-    const int64_t wg = std::min<int64_t>((a.n_units + 3) / 4, 1024);
-    const dim3 grid((unsigned)wg), block(256);
+    const dim3 block(256);
+    if (a.blocks_per_row > 0) {   // direct form: one wave per padded (row, block, head)
+        const int64_t units = (int64_t)a.num_rows * a.blocks_per_row * a.num_kv_heads;
+        AppendArgs d = a;
+        d.n_units = units;
+        const dim3 grid((unsigned)((units + 3) / 4));
+        if (head_dim == 64 && !fp8) hipLaunchKernelGGL((append_rows_kernel<64, false>), grid, block, 0, s, d);
+        else if (head_dim == 64) hipLaunchKernelGGL((append_rows_kernel<64, true>), grid, block, 0, s, d);
+        else if (!fp8) hipLaunchKernelGGL((append_rows_kernel<128, false>), grid, block, 0, s, d);
+        else hipLaunchKernelGGL((append_rows_kernel<128, true>), grid, block, 0, s, d);
+        return hipGetLastError();
+    }
+    // one unit per wave where possible; every workgroup scans all rows, so
+    // the grid shrinks as rows grow (waves then loop over units)
+    const int64_t scan_cap = std::max<int64_t>(1024, (int64_t(1) << 22) / (a.num_rows + 1));
+    const int64_t wg = std::min<int64_t>((a.n_units + 3) / 4, scan_cap);
+    const dim3 grid((unsigned)wg);
     if (head_dim == 64 && !fp8) hipLaunchKernelGGL((append_kernel<64, false>), grid, block, 0, s, a);
     else if (head_dim == 64) hipLaunchKernelGGL((append_kernel<64, true>), grid, block, 0, s, a);
     else if (!fp8) hipLaunchKernelGGL((append_kernel<128, false>), grid, block, 0, s, a);

@@ -14,6 +14,7 @@ struct AppendArgs {
     const int32_t *block_tables, *seq_lens, *q_start;
     int32_t num_rows, num_blocks, num_kv_heads, max_blocks_per_row;
     int64_t n_units;                // upper bound of (row, written block, head) units
+    int32_t blocks_per_row;         // > 0: direct form, written blocks per row bound
 };
 
 struct BlockCopyArgs {

@@ -93,6 +93,28 @@ def test_many_rows(torch_cuda, kv):
     _check_small(w, torch_cuda, f"many-rows-{kv}")
 
 
+def _rows_case(name, n_decode, prefill_q, kv, seed):
+    g = np.random.Generator(np.random.PCG64(seed))
+    rows = [W.RowSpec(W.DECODE, int(g.integers(0, 80)), 1, int(g.integers(-1, 2)))
+            for _ in range(n_decode)]
+    if prefill_q:
+        rows.insert(n_decode // 2, W.RowSpec(W.PREFILL, 40, prefill_q))
+    return W.build(name, rows, {0: 32, 1: 48}, 4, 2, 64, kv_dtype=kv, seed=seed)
+
+
+@pytest.mark.parametrize("kv", [W.KV_BF16, W.KV_FP8])
+def test_append_direct_form(torch_cuda, kv):
+    # decode rows only: every row writes one block, the padded per-row grid is used
+    _check_small(_rows_case(f"direct-{kv}", 300, 0, kv, 115), torch_cuda, f"append-direct-{kv}")
+
+
+@pytest.mark.parametrize("kv", [W.KV_BF16, W.KV_FP8])
+def test_append_scan_form(torch_cuda, kv):
+    # one long prefill row among 2,600 rows: the padded grid would be large, so
+    # units are enumerated by the LDS scan, over two row windows
+    _check_small(_rows_case(f"scan-{kv}", 2600, 600, kv, 116), torch_cuda, f"append-scan-{kv}")
+
+
 def test_deterministic(torch_cuda):
     w = W.random_case(110, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
                       max_ctx=2000, max_q=64)
