@@ -909,15 +909,17 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         for (int t = 0; t < 2; ++t) {
             sc[t][0] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
             sc[t][1] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-            const uint8_t *krow = kl + (32 * ch + ksel_row + 4 * t) * (2 * D);
+        }
 #pragma unroll
-            for (int c = 0; c < NC; ++c) {
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+                const uint8_t *krow = kl + (32 * ch + ksel_row + 4 * t) * (2 * D);
                 const bf16x8_t kf = *(const bf16x8_t *)(krow + 16 * ((4 * c + g4) ^ kswz_lane));
 #pragma unroll
                 for (int nn = 0; nn < 2; ++nn)
                     sc[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], sc[t][nn], 0, 0, 0);
             }
-        }
     };
     const float f = FP8 ? 1.f : scale;  // raw score -> log2 units (e4m3 scales first)
     // scale (e4m3), mask, and the chunk max per query column in log2 units
