@@ -159,6 +159,41 @@ typedef struct {
 int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
                          int32_t num_q_heads, echo_plan_stats_t *stats);
 
+/* The work plan echo_attn_mixed uploads for a batch (host-only; for tests
+ * and tools that inspect plans).  Regions are in 32-bit words from the start
+ * of the workspace; everything below upload_words is the packed plan:
+ *   desc      [n_desc][8]   decode work: tok_off, nt | 1 << 16 when other
+ *                           waves read the same keys, bt_row, key_begin,
+ *                           key_end, part (first partial slot or -1), 0, 0
+ *   pdesc     [n_pdesc][8]  prefill work: row, tok0, ntok, key_end,
+ *                           key_begin, part, kfull (keys every token of the
+ *                           tile sees), 0
+ *   tok_list  [n_tok_list]  tokens of the decode slices
+ *   klim      [n_tokens]    keys visible to each token
+ *   merge_tok [n_merge_rows], merge_ptr [n_merge_rows + 1]
+ *   merge_ent [n_merge_entries][2]  (first slot, nt | i << 10): query i of a
+ *                           slice of nt tokens; the (token, head h) result of
+ *                           an entry sits in slot first + (h / G * head_chunks
+ *                           + (h % G) / 16) * nt * heads_per_chunk + i * nh
+ *                           + (h % G) % 16, nh = min(heads_per_chunk, G - 16 *
+ *                           ((h % G) / 16)), G = Hq / Hkv
+ * Decode descriptor d expands to waves (d, KV head k, head chunk c), whose
+ * partial slots start at part + (k * head_chunks + c) * nt * heads_per_chunk. */
+typedef struct {
+    int64_t n_desc, n_pdesc, n_tok_list, n_tokens, n_merge_rows, n_merge_entries, n_slots;
+    int64_t off_desc, off_pdesc, off_tok_list, off_klim, off_merge_tok, off_merge_ptr,
+        off_merge_ent;
+    int64_t upload_words, off_part_lse, off_part_o, total_words;
+    int32_t head_chunks, heads_per_chunk;
+} echo_plan_layout_t;
+
+/* Fills *layout and, when words is not NULL, packs the plan into the host
+ * buffer words (at least layout->upload_words * 4 bytes, else
+ * ECHO_E_WORKSPACE).  Validates like echo_attn_mixed; no GPU work. */
+int echo_attn_plan_pack(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                        int32_t num_q_heads, echo_plan_layout_t *layout, void *words,
+                        size_t bytes);
+
 /* Host-only validation of pool and batch as echo_kv_append (for_append = 1)
  * or echo_attn_mixed (for_append = 0) would do it; no GPU work. */
 int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t for_append);

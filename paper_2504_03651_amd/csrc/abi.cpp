@@ -3,6 +3,7 @@
 #include <hip/hip_runtime_api.h>
 
 #include <algorithm>
+#include <atomic>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -161,6 +162,23 @@ PlanOptions plan_options() {
         return v > 0 ? v : 48;
     }();
     o.split_blocks = split;
+    // compute units of the current device (256 on MI355X; also the value
+    // used by host-only calls made where no device is present)
+    static std::atomic<int> cus[64];
+    int dev = 0;
+    if (hipGetDevice(&dev) == hipSuccess && dev >= 0 && dev < 64) {
+        int v = cus[dev].load(std::memory_order_relaxed);
+        if (v == 0) {
+            if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess ||
+                v <= 0)
+                v = 256;
+            cus[dev].store(v, std::memory_order_relaxed);
+        }
+        o.num_cus = v;
+    } else {
+        (void)hipGetLastError();
+        o.num_cus = 256;
+    }
     return o;
 }
 
@@ -451,6 +469,43 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
     return ECHO_OK;
 }
 
+int echo_attn_plan_pack(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                        int32_t num_q_heads, echo_plan_layout_t *layout, void *words,
+                        size_t bytes) {
+    g_error.clear();
+    if (!layout) return fail(ECHO_E_INVALID, "layout is NULL");
+    thread_local Plan plan;
+    int rc = plan_for(pool, batch, num_q_heads, plan);
+    if (rc) return rc;
+    const PlanLayout &L = plan.layout;
+    layout->n_desc = L.n_desc;
+    layout->n_pdesc = L.n_pdesc;
+    layout->n_tok_list = L.n_tok_list;
+    layout->n_tokens = L.n_tokens;
+    layout->n_merge_rows = L.n_merge_rows;
+    layout->n_merge_entries = L.n_merge_entries;
+    layout->n_slots = L.n_slots;
+    layout->off_desc = L.off_desc;
+    layout->off_pdesc = L.off_pdesc;
+    layout->off_tok_list = L.off_tok_list;
+    layout->off_klim = L.off_klim;
+    layout->off_merge_tok = L.off_merge_tok;
+    layout->off_merge_ptr = L.off_merge_ptr;
+    layout->off_merge_ent = L.off_merge_ent;
+    layout->upload_words = L.upload_words;
+    layout->off_part_lse = L.off_part_lse;
+    layout->off_part_o = L.off_part_o;
+    layout->total_words = L.total_words;
+    layout->head_chunks = plan.head_chunks;
+    layout->heads_per_chunk = plan.heads_per_chunk;
+    if (!words) return ECHO_OK;
+    if (bytes < (size_t)L.upload_words * 4)
+        return fail(ECHO_E_WORKSPACE, "plan buffer of %zu bytes, need %lld", bytes,
+                    (long long)L.upload_words * 4);
+    pack_plan(plan, words);
+    return ECHO_OK;
+}
+
 int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
                     int32_t num_q_heads, float sm_scale, float *out, void *workspace,
                     size_t workspace_bytes, void *stream) {
@@ -467,7 +522,7 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
         return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
     int32_t pf_blocks = 0;
     for (const PrefillDesc &d : plan.pdesc)
-        pf_blocks = std::max(pf_blocks, (d.key_end + kBlock - 1) / kBlock);
+        pf_blocks = std::max(pf_blocks, (d.key_end + kBlock - 1) / kBlock - d.key_begin / kBlock);
     if (pf_blocks > prefill_max_blocks(pool->head_dim))
         return fail(ECHO_E_UNSUPPORTED, "prefill row of %d blocks exceeds the %d-block limit",
                     pf_blocks, prefill_max_blocks(pool->head_dim));
@@ -542,6 +597,10 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     pf.scale_log2 = a.scale_log2;
     pf.out = out;
     pf.max_blocks = pf_blocks;
+    pf.head_chunks = plan.head_chunks;
+    pf.heads_per_chunk = plan.heads_per_chunk;
+    pf.part_o = a.part_o;
+    pf.part_lse = a.part_lse;
     hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s,
                                     ev ? ev + 2 : nullptr);
     if (e != hipSuccess) return hip_fail(e, "attention launch");

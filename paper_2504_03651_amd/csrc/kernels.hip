@@ -758,6 +758,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     const int tok0 = __builtin_amdgcn_readfirstlane(dp[1]);
     const int ntok = __builtin_amdgcn_readfirstlane(dp[2]);
     const int key_end = __builtin_amdgcn_readfirstlane(dp[3]);
+    const int key_begin = __builtin_amdgcn_readfirstlane(dp[4]);   // piece of the keys
+    const int part = __builtin_amdgcn_readfirstlane(dp[5]);        // >= 0: partial results
+    const int kfull = __builtin_amdgcn_readfirstlane(dp[6]);       // keys every token sees
 
     const int tid = threadIdx.x;
     const int lane = tid & 63;
@@ -805,17 +808,17 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     const int64_t blk_stride = (int64_t)a.num_kv_heads * 16 * D;
     const KT *kbase = (const KT *)a.k + (int64_t)kvh * 16 * D;
     const KT *vbase = (const KT *)a.v + (int64_t)kvh * 16 * D;
-    const int ntiles = (key_end + kPfKeys - 1) / kPfKeys;
-    const int nblk = (key_end + 15) / 16;
+    const int ntiles = (key_end + kPfKeys - 1) / kPfKeys;   // tiles kt0 .. ntiles-1 of the row
+    const int kt0 = key_begin / kPfKeys;
+    const int kb0 = key_begin / 16, nblk = (key_end + 15) / 16 - kb0;   // blocks staged
     // keys every query of the workgroup sees: tiles below this need no mask
-    const int kfull = key_end - ntok + 1;
 
     // The row's block ids (up to the last key of the tile) are staged in LDS
     // once; tile block indices past the last block are clamped so that every
     // copy is unconditional (keys past key_end are zeroed or masked instead).
-    for (int e = tid; e < nblk; e += kPfThreads) lids[e] = btr[e];
+    for (int e = tid; e < nblk; e += kPfThreads) lids[e] = btr[kb0 + e];
     __syncthreads();
-    auto blk_of = [&](int kt, int b) -> int { return lids[min(4 * kt + b, nblk - 1)]; };
+    auto blk_of = [&](int kt, int b) -> int { return lids[min(4 * (kt - kt0) + b, nblk - 1)]; };
 
     // This wave's NJ copies of a tile all fall in block `bsel` of the tile's
     // four; per lane, where each 16-byte piece comes from inside the block is
@@ -833,7 +836,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 3) & 1);
         v_off[j] = d * 16 + 8 * h;
     }
-    auto tile_id = [&](int kt) -> int { return lids[min(4 * kt + bsel, nblk - 1)]; };
+    auto tile_id = [&](int kt) -> int { return lids[min(4 * (kt - kt0) + bsel, nblk - 1)]; };
 
     Raw kreg[FP8 ? NJ : 1], vreg[FP8 ? NJ : 1];
     float sreg = 0.f;
@@ -1058,42 +1061,43 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // registers during tile kt and widened into LDS before the barrier.
     constexpr int LA = (FP8 || kPfStages == 2) ? 1 : 2;  // tiles in flight ahead
     const int tail_tile = (kPfKeys * ntiles > key_end) ? ntiles - 1 : -1;
-    issue_tile(0, 0, tile_id(0));
+    // LDS buffer of tile kt: (kt - kt0) % kPfStages
+    issue_tile(kt0, 0, tile_id(kt0));
     store_tile(0);
-    if (LA == 2 && ntiles > 1) issue_tile(1, 1, tile_id(1));
-    int id_ahead = tile_id(LA);   // block id of the next tile to issue
-    if (LA == 2 && ntiles > 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
+    if (LA == 2 && ntiles > kt0 + 1) issue_tile(kt0 + 1, 1, tile_id(kt0 + 1));
+    int id_ahead = tile_id(kt0 + LA);   // block id of the next tile to issue
+    if (LA == 2 && ntiles > kt0 + 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
     else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
     __builtin_amdgcn_s_barrier();
-    if (tail_tile == 0) {
-        zero_tail(0, 0);
+    if (tail_tile == kt0) {
+        zero_tail(kt0, 0);
         __syncthreads();
     }
 
     auto step = [&](int kt, bool masked) {
-        const int buf = kt % kPfStages;
+        const int buf = (kt - kt0) % kPfStages;
         bool ahead = false;   // copies of tile kt+2 issued after those of kt+1
         if (kt + LA < ntiles) {
-            issue_tile(kt + LA, (kt + LA) % kPfStages, id_ahead);
+            issue_tile(kt + LA, (kt + LA - kt0) % kPfStages, id_ahead);
             ahead = LA == 2;
         }
         id_ahead = tile_id(kt + LA + 1);
         tile(buf, kt, masked);
         if (kt + 1 < ntiles) {
-            if constexpr (LA == 1) store_tile((kt + 1) % kPfStages);
+            if constexpr (LA == 1) store_tile((kt + 1 - kt0) % kPfStages);
             if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
             else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
             __builtin_amdgcn_s_barrier();
             if (kt + 1 == tail_tile) {
-                zero_tail(kt + 1, (kt + 1) % kPfStages);
+                zero_tail(kt + 1, (kt + 1 - kt0) % kPfStages);
                 __syncthreads();
             }
         }
     };
     // tiles every query sees in full, then the diagonal tiles with the mask
     const int nfull = min(kfull / kPfKeys, ntiles);
-    for (int kt = 0; kt < nfull; ++kt) step(kt, false);
-    for (int kt = nfull; kt < ntiles; ++kt) step(kt, true);
+    for (int kt = kt0; kt < nfull; ++kt) step(kt, false);
+    for (int kt = max(nfull, kt0); kt < ntiles; ++kt) step(kt, true);
 
 #pragma unroll
     for (int nn = 0; nn < 2; ++nn) {
@@ -1106,7 +1110,20 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         }
         if (!qok[nn]) continue;
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
-        float *dst = a.out + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 4 * g4;
+        float *dst;
+        if (part < 0) {
+            dst = a.out + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 4 * g4;
+        } else {
+            // the slot the merge kernel reads for (token, head) of this piece:
+            // part + (kvh * head_chunks + hc) * ntok * heads_per_chunk + token * nh + jh
+            const int qi = 32 * wave + 16 * nn + c16, tl = qi / G, hg = qi - tl * G;
+            const int hc = hg / 16, jh = hg - 16 * hc;
+            const int nh = min(a.heads_per_chunk, G - 16 * hc);
+            const int64_t slot = part + (int64_t)(kvh * a.head_chunks + hc) * ntok * a.heads_per_chunk +
+                                 (int64_t)tl * nh + jh;
+            dst = a.part_o + slot * D + 4 * g4;
+            if (g4 == 0) a.part_lse[slot] = l_tot > 0.f ? m_run[nn] + log2f(l_tot) : -INFINITY;
+        }
 #pragma unroll
         for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i) = acc[nn][i] * inv;
     }
@@ -1142,7 +1159,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
         float lse = -INFINITY;
         if (e < e1) {
             const int part = a.merge_ent[2 * e], sh = a.merge_ent[2 * e + 1];
-            slot = part + rem * (sh & 0xFF) * a.heads_per_chunk + (sh >> 8) * nh + jh;
+            slot = part + rem * (sh & 0x3FF) * a.heads_per_chunk + (sh >> 10) * nh + jh;
             lse = a.part_lse[slot];
         }
         float bm = lse;

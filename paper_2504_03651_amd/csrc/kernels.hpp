@@ -57,7 +57,9 @@ struct PrefillArgs {
     int32_t max_blocks_per_row;
     float scale_log2;
     float *out;
-    int32_t max_blocks;             // most blocks any tile's row reads (ids staged in LDS)
+    int32_t max_blocks;             // most blocks any piece reads (ids staged in LDS)
+    int32_t head_chunks, heads_per_chunk;   // partial-slot layout shared with decode
+    float *part_o, *part_lse;       // partial results of pieces of split key ranges
 };
 
 struct MergeArgs {

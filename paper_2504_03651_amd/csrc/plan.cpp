@@ -137,7 +137,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         for (int32_t k = 0; k < s.nrows; ++k) cnt[seg_rows[s.rows_off + k]] += n_splits(s);
 
     // merge lists: rows with more than one contribution; entries
-    // (first partial slot of the descriptor, nt | i << 8) for query i of a
+    // (first partial slot of the descriptor, nt | i << 10) for query i of a
     // slice of nt tokens
     moff.assign((size_t)B, -1);
     int64_t n_ent = 0;
@@ -181,7 +181,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
                         const int32_t m = moff[seg_rows[s.rows_off + k0 + i]];
                         const int64_t e = plan.merge_ptr[m] + cursor[m]++;
                         plan.merge_ent[2 * e] = d.part;
-                        plan.merge_ent[2 * e + 1] = ntk | (i << 8);
+                        plan.merge_ent[2 * e + 1] = ntk | (i << 10);
                     }
                     n_slots += wpd * ntk * hpc;
                 }
@@ -197,6 +197,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     plan.pdesc.clear();
     const int32_t bt_tok = std::max(1, kPrefillQueries / G);
     plan.prefill_tokens_per_tile = bt_tok;
+    int64_t pf_work = 0, pf_tiles = 0;   // 64-key tiles summed over the prefill tiles
     for (int32_t r = 0; r < B; ++r) {
         if (b.kind[r] != ECHO_ROW_PREFILL) continue;
         const int32_t q = b.q_start[r + 1] - b.q_start[r];
@@ -208,10 +209,67 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             d.tok0 = b.q_start[r] + k * bt_tok;
             d.ntok = std::min(bt_tok, q - k * bt_tok);
             d.key_end = c + k * bt_tok + d.ntok;
+            d.key_begin = 0;
+            d.part = -1;
+            d.kfull = d.key_end - d.ntok + 1;
+            d.pad0 = 0;
             plan.pdesc.push_back(d);
-            plan.stats.prefill_items += Hkv;
+            pf_work += (d.key_end + kPrefillTileKeys - 1) / kPrefillTileKeys;
+            ++pf_tiles;
         }
     }
+    // Fewer than two workgroups per CU leave most CUs idle while the longest
+    // tiles finish: cut key ranges longer than the average share of a CU into
+    // pieces at tile boundaries that every token of the tile sees unmasked.
+    // Pieces write partial softmax states that the merge kernel combines.
+    if (pf_tiles > 0 && pf_tiles * Hkv < 2 * (int64_t)opt.num_cus) {
+        const int64_t share = (pf_work * Hkv + opt.num_cus - 1) / opt.num_cus;
+        const int32_t piece = (int32_t)std::max<int64_t>(kPrefillMinPieceTiles, share);
+        std::vector<PrefillDesc> &out = plan.pdesc_split;
+        out.clear();
+        if (!plan.merge_ptr.empty()) plan.merge_ptr.pop_back();   // reopen the list
+        for (const PrefillDesc &d : plan.pdesc) {
+            const int32_t nt = (d.key_end + kPrefillTileKeys - 1) / kPrefillTileKeys;
+            const int32_t unmasked = d.kfull / kPrefillTileKeys;   // whole tiles every token sees
+            int32_t cut = 0;
+            std::vector<int32_t> &bounds = plan.bounds;
+            bounds.assign(1, 0);
+            while (nt - cut > piece && cut + piece <= unmasked) {
+                cut += piece;
+                bounds.push_back(cut);
+            }
+            if (bounds.size() == 1) {
+                out.push_back(d);
+                continue;
+            }
+            bounds.push_back(nt);
+            const int32_t slots = Hkv * nhc * d.ntok * hpc;
+            for (int32_t i = 0; i < d.ntok; ++i) {
+                plan.merge_tok.push_back(d.tok0 + i);
+                plan.merge_ptr.push_back((int32_t)(plan.merge_ent.size() / 2));
+                for (size_t p = 0; p + 1 < bounds.size(); ++p) {
+                    plan.merge_ent.push_back((int32_t)(n_slots + (int64_t)p * slots));
+                    plan.merge_ent.push_back(d.ntok | (i << 10));
+                }
+            }
+            for (size_t p = 0; p + 1 < bounds.size(); ++p) {
+                PrefillDesc e = d;
+                e.key_begin = bounds[p] * kPrefillTileKeys;
+                e.key_end = p + 2 < bounds.size() ? bounds[p + 1] * kPrefillTileKeys : d.key_end;
+                e.part = (int32_t)(n_slots + (int64_t)p * slots);
+                out.push_back(e);
+            }
+            n_slots += (int64_t)(bounds.size() - 1) * slots;
+        }
+        plan.merge_ptr.push_back((int32_t)(plan.merge_ent.size() / 2));
+        // longest pieces first
+        std::stable_sort(out.begin(), out.end(), [](const PrefillDesc &x, const PrefillDesc &y) {
+            return x.key_end - x.key_begin > y.key_end - y.key_begin;
+        });
+        plan.pdesc.swap(out);
+    }
+    plan.stats.prefill_items = (int64_t)plan.pdesc.size() * Hkv;
+    n_ent = (int64_t)plan.merge_ent.size() / 2;
 
     // heavy descriptors first (counting sort on 32-key steps, stable)
     {
@@ -242,8 +300,9 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     L.n_slots = n_slots;
     int64_t w = 0;
     L.n_pdesc = (int64_t)plan.pdesc.size();
-    L.off_desc = w;       w += L.n_desc * 8;
-    L.off_pdesc = w;      w += L.n_pdesc * 4;
+    static_assert(sizeof(WorkDesc) % 4 == 0 && sizeof(PrefillDesc) % 4 == 0, "word-sized descriptors");
+    L.off_desc = w;       w += L.n_desc * (int64_t)(sizeof(WorkDesc) / 4);
+    L.off_pdesc = w;      w += L.n_pdesc * (int64_t)(sizeof(PrefillDesc) / 4);
     L.off_tok_list = w;   w += L.n_tok_list;
     L.off_klim = w;       w += L.n_tokens;
     L.off_merge_tok = w;  w += L.n_merge_rows;

@@ -47,13 +47,19 @@ static_assert(sizeof(WorkDesc) == 32, "descriptor layout");
 #define ECHO_PF_WAVES 8
 #endif
 constexpr int kPrefillQueries = 32 * ECHO_PF_WAVES;
-struct PrefillDesc {   // 16 bytes
+struct PrefillDesc {   // 32 bytes
     int32_t row;
     int32_t tok0;      // first token of the tile
     int32_t ntok;      // tokens in the tile
-    int32_t key_end;   // keys visible to the last token
+    int32_t key_end;   // one past the last key of this piece of the tile's keys
+    int32_t key_begin; // first key of the piece, a multiple of the 64-key tile
+    int32_t part;      // first partial slot of the piece, or -1: write `out`
+    int32_t kfull;     // keys every token of the tile sees (unmasked below)
+    int32_t pad0;
 };
-static_assert(sizeof(PrefillDesc) == 16, "prefill descriptor layout");
+static_assert(sizeof(PrefillDesc) == 32, "prefill descriptor layout");
+constexpr int kPrefillTileKeys = 64;      // keys per LDS tile of the prefill kernel
+constexpr int kPrefillMinPieceTiles = 8;  // shortest piece a long key range is cut into
 
 // Wave w of the attention grid handles descriptor w / (Hkv * head_chunks),
 // KV head (w % (Hkv * head_chunks)) / head_chunks and head chunk
@@ -76,7 +82,7 @@ struct PlanLayout {
     int64_t off_klim = 0;       // int32[n_tokens]: keys visible to each token
     int64_t off_merge_tok = 0;  // int32[n_merge_rows]: the row's token
     int64_t off_merge_ptr = 0;  // int32[n_merge_rows + 1]
-    int64_t off_merge_ent = 0;  // int32[2 * n_merge_entries]: (first slot, nt | i << 8)
+    int64_t off_merge_ent = 0;  // int32[2 * n_merge_entries]: (first slot, nt | i << 10)
     int64_t upload_words = 0;   // everything above is uploaded
     int64_t off_part_lse = 0;   // float[n_slots]
     int64_t off_part_o = 0;     // float[n_slots][head_dim]
@@ -97,12 +103,15 @@ struct HostBatch {
 
 struct PlanOptions {
     int split_blocks = 48;  // key blocks per decode split
+    int num_cus = 256;      // compute units: prefill key ranges are cut into
+                            // pieces when there are fewer than two workgroups per CU
 };
 
 // Host plan under construction (reused between calls on the same thread).
 struct Plan {
     std::vector<WorkDesc> desc, desc_sorted;
-    std::vector<PrefillDesc> pdesc;
+    std::vector<PrefillDesc> pdesc, pdesc_split;
+    std::vector<int32_t> bounds;
     int32_t prefill_tokens_per_tile = 1;
     std::vector<int32_t> tok_list, klim, merge_tok, merge_ptr, merge_ent;
     // scratch

@@ -26,7 +26,8 @@ KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
 SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes", "echo_block_copy",
-           "echo_attn_plan_stats", "echo_validate", "echo_status_string", "echo_last_error",
+           "echo_attn_plan_stats", "echo_attn_plan_pack", "echo_validate", "echo_status_string",
+           "echo_last_error",
            "echo_profile", "echo_attn_timing"]
 
 
@@ -61,6 +62,14 @@ class CPlanStats(ctypes.Structure):
         "decode_kv_tokens", "prefill_causal_pairs", "workspace_bytes")]
 
 
+class CPlanLayout(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int64) for n in (
+        "n_desc", "n_pdesc", "n_tok_list", "n_tokens", "n_merge_rows", "n_merge_entries", "n_slots",
+        "off_desc", "off_pdesc", "off_tok_list", "off_klim", "off_merge_tok", "off_merge_ptr",
+        "off_merge_ent", "upload_words", "off_part_lse", "off_part_o", "total_words")] + [
+        ("head_chunks", ctypes.c_int32), ("heads_per_chunk", ctypes.c_int32)]
+
+
 class CAttnTiming(ctypes.Structure):
     _fields_ = [(n, ctypes.c_float) for n in ("upload_ms", "prefill_ms", "decode_ms", "merge_ms")]
 
@@ -84,6 +93,8 @@ def lib():
         L.echo_attn_workspace_bytes.restype = ctypes.c_size_t
         L.echo_block_copy.argtypes = [P, vp, ctypes.c_int32, vp, vp]
         L.echo_attn_plan_stats.argtypes = [P, B, ctypes.c_int32, ctypes.POINTER(CPlanStats)]
+        L.echo_attn_plan_pack.argtypes = [P, B, ctypes.c_int32, ctypes.POINTER(CPlanLayout), vp,
+                                          ctypes.c_size_t]
         L.echo_validate.argtypes = [P, B, ctypes.c_int32]
         L.echo_status_string.argtypes = [ctypes.c_int]
         L.echo_status_string.restype = ctypes.c_char_p
@@ -94,7 +105,7 @@ def lib():
         L.echo_attn_timing.argtypes = [ctypes.POINTER(CAttnTiming)]
         L.echo_attn_timing.restype = ctypes.c_int
         for name in ("echo_kv_append", "echo_attn_mixed", "echo_block_copy",
-                     "echo_attn_plan_stats", "echo_validate"):
+                     "echo_attn_plan_stats", "echo_attn_plan_pack", "echo_validate"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -230,6 +241,18 @@ def plan_stats(cpool: CPool, cbatch: CBatch, num_q_heads: int) -> dict:
     _check(lib().echo_attn_plan_stats(ctypes.byref(cpool), ctypes.byref(cbatch),
                                       int(num_q_heads), ctypes.byref(st)), "echo_attn_plan_stats")
     return {name: int(getattr(st, name)) for name, _ in CPlanStats._fields_}
+
+
+def plan_pack(cpool: CPool, cbatch: CBatch, num_q_heads: int):
+    """(layout dict, int32 words) of the plan echo_attn_mixed would upload."""
+    lay = CPlanLayout()
+    _check(lib().echo_attn_plan_pack(ctypes.byref(cpool), ctypes.byref(cbatch), int(num_q_heads),
+                                     ctypes.byref(lay), None, 0), "echo_attn_plan_pack")
+    words = np.zeros(max(int(lay.upload_words), 1), np.int32)
+    _check(lib().echo_attn_plan_pack(ctypes.byref(cpool), ctypes.byref(cbatch), int(num_q_heads),
+                                     ctypes.byref(lay), words.ctypes.data, words.nbytes),
+           "echo_attn_plan_pack")
+    return {name: int(getattr(lay, name)) for name, _ in CPlanLayout._fields_}, words
 
 
 def profile(enable: bool) -> bool:

@@ -115,6 +115,17 @@ def test_append_scan_form(torch_cuda, kv):
     _check_small(_rows_case(f"scan-{kv}", 2600, 600, kv, 116), torch_cuda, f"append-scan-{kv}")
 
 
+@pytest.mark.parametrize("hq,hkv,d,kv", [(32, 1, 64, W.KV_BF16), (8, 2, 128, W.KV_FP8),
+                                         (4, 4, 128, W.KV_BF16)])
+def test_prefill_split_key_ranges(torch_cuda, hq, hkv, d, kv):
+    # few prefill tiles with long cached contexts: their key ranges are cut
+    # into pieces whose partial results the merge kernel combines
+    rows = [W.RowSpec(W.PREFILL, 3000, 40), W.RowSpec(W.DECODE, 700, 1),
+            W.RowSpec(W.PREFILL, 1500, 300), W.RowSpec(W.PREFILL, 64, 17)]
+    w = W.build(f"split-{hq}-{hkv}-{d}-{kv}", rows, {}, hq, hkv, d, kv_dtype=kv, seed=118)
+    _check_small(w, torch_cuda, f"prefill-split-{hq}/{hkv}/{d}/{kv}")
+
+
 def test_deterministic(torch_cuda):
     w = W.random_case(110, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
                       max_ctx=2000, max_q=64)

@@ -1,0 +1,183 @@
+"""Host-side invariants of the work plan that echo_attn_mixed uploads (CPU).
+
+The plan is packed by the library's own code (echo_attn_plan_pack) and
+decoded here word by word, so that a layout or planning mistake shows up on
+the CPU instead of as a wrong address on the GPU:
+  * the regions fit inside the workspace without overlapping;
+  * every descriptor names valid rows, tokens, key ranges and partial slots;
+  * for every new token, the key ranges of the work items that cover it tile
+    [0, keys visible to it) exactly once, and a token with several items has
+    one merge row whose entries are exactly those items;
+  * partial-slot ranges of different items never overlap.
+"""
+import numpy as np
+import pytest
+
+from paper_2504_03651_amd import echo
+from paper_2504_03651_amd import workload as W
+
+TILE = 64   # keys per prefill LDS tile
+
+
+def _cases():
+    yield W.config1()
+    yield W.config1(share_with_prefill=True)
+    for seed in (201, 202, 203):
+        yield W.random_case(seed, num_rows=9, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                            max_ctx=2500, max_q=120, n_groups=3)
+    yield W.random_case(204, num_rows=7, num_q_heads=32, num_kv_heads=1, head_dim=64,
+                        max_ctx=3000, max_q=60, n_groups=2)
+    for hq, hkv in ((32, 1), (8, 2), (4, 4)):
+        rows = [W.RowSpec(W.PREFILL, 3000, 40), W.RowSpec(W.DECODE, 700, 1),
+                W.RowSpec(W.PREFILL, 1500, 300), W.RowSpec(W.PREFILL, 64, 17)]
+        yield W.build(f"split-{hq}-{hkv}", rows, {}, hq, hkv, 128, seed=118)
+    yield W.config(3)
+    yield W.random_case(205, num_rows=600, num_q_heads=4, num_kv_heads=2, head_dim=64,
+                        max_ctx=100, max_q=30, n_groups=3)
+
+
+CASES = list(_cases())
+
+
+def _decode(w):
+    cp, cb, _keep = echo.host_structs(w)
+    lay, words = echo.plan_pack(cp, cb, w.num_q_heads)
+    return lay, words
+
+
+@pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
+def test_plan_invariants(w):
+    lay, words = _decode(w)
+    b = w.batch
+    B, T = b.num_rows, b.num_tokens
+    Hq, Hkv = w.num_q_heads, w.num_kv_heads
+    G = Hq // Hkv
+    hpc, nhc = lay["heads_per_chunk"], lay["head_chunks"]
+    assert hpc == min(G, 16) and nhc == (G + 15) // 16
+
+    # ---- regions in order, inside the workspace
+    ends = [
+        ("desc", lay["off_desc"], 8 * lay["n_desc"]),
+        ("pdesc", lay["off_pdesc"], 8 * lay["n_pdesc"]),
+        ("tok_list", lay["off_tok_list"], lay["n_tok_list"]),
+        ("klim", lay["off_klim"], lay["n_tokens"]),
+        ("merge_tok", lay["off_merge_tok"], lay["n_merge_rows"]),
+        ("merge_ptr", lay["off_merge_ptr"], lay["n_merge_rows"] + 1),
+        ("merge_ent", lay["off_merge_ent"], 2 * lay["n_merge_entries"]),
+    ]
+    pos = 0
+    for name, off, n in ends:
+        assert off >= pos, f"{name} overlaps the region before it"
+        pos = off + n
+    assert pos <= lay["upload_words"] <= lay["off_part_lse"]
+    assert lay["off_part_lse"] + lay["n_slots"] <= lay["off_part_o"]
+    assert lay["off_part_o"] + lay["n_slots"] * w.head_dim <= lay["total_words"]
+    assert lay["n_tokens"] == T
+
+    def region(off, n, width=1):
+        return words[off:off + n * width].reshape(n, width) if width > 1 else words[off:off + n]
+
+    desc = region(lay["off_desc"], lay["n_desc"], 8)
+    pdesc = region(lay["off_pdesc"], lay["n_pdesc"], 8)
+    tok_list = region(lay["off_tok_list"], lay["n_tok_list"])
+    klim = region(lay["off_klim"], T)
+    mtok = region(lay["off_merge_tok"], lay["n_merge_rows"])
+    mptr = region(lay["off_merge_ptr"], lay["n_merge_rows"] + 1)
+    ment = region(lay["off_merge_ent"], lay["n_merge_entries"], 2)
+
+    # ---- per-token keys and rows
+    q = np.diff(b.q_start)
+    row_of = np.repeat(np.arange(B), q)
+    pos_of = np.concatenate([b.seq_lens[r] - q[r] + np.arange(q[r]) for r in range(B)]) \
+        if B else np.zeros(0, np.int64)
+    assert np.array_equal(klim, pos_of + 1)
+
+    ranges = [[] for _ in range(T)]        # (begin, end, part, slice size, index)
+    slot_ranges = []
+    for d in desc:
+        tok_off, shape, bt_row, kb, ke, part = (int(x) for x in d[:6])
+        nt = shape & 0xFF
+        assert 1 <= nt <= 16 // hpc * max(1, 1) or nt <= 16
+        assert 0 <= tok_off and tok_off + nt <= len(tok_list)
+        assert 0 <= bt_row < B and b.row_kind[bt_row] == W.DECODE
+        assert kb % 16 == 0 and 0 <= kb < ke <= b.seq_lens[bt_row]
+        for i in range(nt):
+            t = int(tok_list[tok_off + i])
+            r = row_of[t]
+            assert b.row_kind[r] == W.DECODE
+            # the slice reads bt_row's blocks for these keys: they must be this row's too
+            j0, j1 = kb // 16, (ke + 15) // 16
+            assert ke <= b.seq_lens[r]
+            assert np.array_equal(b.block_tables[r, j0:j1], b.block_tables[bt_row, j0:j1])
+            ranges[t].append((kb, ke, part, nt, i))
+        if part >= 0:
+            slot_ranges.append((part, part + Hkv * nhc * nt * hpc))
+    for d in pdesc:
+        row, tok0, ntok, ke, kb, part, kfull = (int(x) for x in d[:7])
+        assert b.row_kind[row] == W.PREFILL
+        assert b.q_start[row] <= tok0 and tok0 + ntok <= b.q_start[row + 1]
+        assert 1 <= ntok <= max(1, 256 // G)
+        assert kb % TILE == 0 and 0 <= kb < ke <= b.seq_lens[row]
+        assert kfull == klim[tok0]
+        # every piece but a tile's last lies in keys all of its tokens see
+        last = ke == klim[tok0 + ntok - 1]
+        assert last or ke <= kfull
+        for i in range(ntok):
+            ranges[tok0 + i].append((kb, min(ke, int(klim[tok0 + i])), part, ntok, i))
+        if part >= 0:
+            slot_ranges.append((part, part + Hkv * nhc * ntok * hpc))
+
+    # ---- coverage: exactly [0, klim) once per token
+    for t in range(T):
+        iv = sorted((kb, ke) for kb, ke, *_ in ranges[t])
+        assert iv, f"token {t} has no work"
+        cur = 0
+        for kb, ke in iv:
+            assert kb == cur, f"token {t}: keys {cur}..{kb} uncovered or overlapping"
+            cur = ke
+        assert cur == klim[t], f"token {t}: keys up to {cur}, visible {klim[t]}"
+
+    # ---- merge rows: tokens with several items, entries exactly those items
+    merged = {int(t): k for k, t in enumerate(mtok)}
+    assert len(merged) == len(mtok), "a token has two merge rows"
+    for t in range(T):
+        items = ranges[t]
+        if len(items) == 1:
+            assert t not in merged and items[0][2] == -1
+            continue
+        assert t in merged, f"token {t} has {len(items)} items but no merge row"
+        k = merged[t]
+        ent = ment[mptr[k]:mptr[k + 1]]
+        want = sorted((part, nt | (i << 10)) for _kb, _ke, part, nt, i in items)
+        assert all(p >= 0 for p, _ in want)
+        assert sorted(map(tuple, ent.tolist())) == want
+
+    # ---- partial slots: disjoint ranges inside n_slots
+    slot_ranges.sort()
+    for (a0, a1), (b0, _b1) in zip(slot_ranges, slot_ranges[1:]):
+        assert a1 <= b0, "two work items share partial slots"
+    if slot_ranges:
+        assert slot_ranges[0][0] >= 0 and slot_ranges[-1][1] <= lay["n_slots"]
+
+
+def test_split_pieces_present():
+    # the split shapes above must actually exercise pieces of key ranges
+    w = W.build("split-check", [W.RowSpec(W.PREFILL, 3000, 40), W.RowSpec(W.DECODE, 700, 1)],
+                {}, 8, 2, 128, seed=118)
+    lay, words = _decode(w)
+    pd = words[lay["off_pdesc"]:lay["off_pdesc"] + 8 * lay["n_pdesc"]].reshape(-1, 8)
+    assert (pd[:, 5] >= 0).any() and (pd[:, 4] > 0).any()
+
+
+def test_plan_pack_buffer_too_small():
+    w = W.config1()
+    cp, cb, _keep = echo.host_structs(w)
+    import ctypes
+    lay = echo.CPlanLayout()
+    L = echo.lib()
+    assert L.echo_attn_plan_pack(ctypes.byref(cp), ctypes.byref(cb), w.num_q_heads,
+                                 ctypes.byref(lay), None, 0) == echo.ECHO_OK
+    buf = np.zeros(4, np.int32)
+    rc = L.echo_attn_plan_pack(ctypes.byref(cp), ctypes.byref(cb), w.num_q_heads,
+                               ctypes.byref(lay), buf.ctypes.data, buf.nbytes)
+    assert rc == echo.ECHO_E_WORKSPACE
