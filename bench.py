@@ -42,6 +42,8 @@ DESCRIPTIONS = {
     4: "long-context: 32 rows at 32,768-token contexts, GQA 64/8, groups of 8 share "
        "16,384-token prefixes, 28 decode + 4 prefill chunks of 4,096",
     5: "config 3 at 4x batch with fp8-e4m3 KV and per-(block, head) fp32 scales",
+    6: "extra shape: a 64-token prefill chunk on 30,000 cached tokens beside 8 decode rows, "
+       "GQA 64/8, D 128 (few prefill tiles: key ranges split across the GPU)",
 }
 
 
@@ -50,7 +52,7 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5])
+    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-pairs", type=int, default=1024)

@@ -218,11 +218,13 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             ++pf_tiles;
         }
     }
-    // Fewer than two workgroups per CU leave most CUs idle while the longest
-    // tiles finish: cut key ranges longer than the average share of a CU into
-    // pieces at tile boundaries that every token of the tile sees unmasked.
-    // Pieces write partial softmax states that the merge kernel combines.
-    if (pf_tiles > 0 && pf_tiles * Hkv < 2 * (int64_t)opt.num_cus) {
+    // Workgroups for at most half the CUs leave the rest idle (a late chunk
+    // of a long prompt is a handful of tiles over tens of thousands of keys):
+    // cut key ranges longer than the average share of a CU into pieces at
+    // tile boundaries that every token of the tile sees unmasked.  Pieces
+    // write partial softmax states that the merge kernel combines.  (With
+    // about one workgroup per CU the merge costs what the balance gains.)
+    if (pf_tiles > 0 && 2 * pf_tiles * Hkv <= (int64_t)opt.num_cus) {
         const int64_t share = (pf_work * Hkv + opt.num_cus - 1) / opt.num_cus;
         const int32_t piece = (int32_t)std::max<int64_t>(kPrefillMinPieceTiles, share);
         std::vector<PrefillDesc> &out = plan.pdesc_split;

@@ -104,7 +104,7 @@ struct HostBatch {
 struct PlanOptions {
     int split_blocks = 48;  // key blocks per decode split
     int num_cus = 256;      // compute units: prefill key ranges are cut into
-                            // pieces when there are fewer than two workgroups per CU
+                            // pieces when workgroups would fill at most half of them
 };
 
 // Host plan under construction (reused between calls on the same thread).

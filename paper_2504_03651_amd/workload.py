@@ -303,8 +303,9 @@ def build(name: str, rows: list, groups: dict, num_q_heads: int, num_kv_heads: i
 
 
 def config(index: int, seed: int | None = None, **kw) -> Workload:
-    """Configurations 1..5 (see the module docstring of each builder)."""
-    fn = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5}[index]
+    """Configurations 1..5 (see the docstring of each builder), and 6, an
+    extra shape: a late prefill chunk of a long prompt."""
+    fn = {1: config1, 2: config2, 3: config3, 4: config4, 5: config5, 6: late_chunk}[index]
     return fn(seed=index if seed is None else seed, **kw)
 
 
@@ -378,6 +379,15 @@ def config5(seed: int = 5, **kw) -> Workload:
     g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
     rows, groups = _mixed_rows(g, 32, 2, 512, 32)
     return build("cfg5-mixed-fp8", rows, groups, 32, 8, 128, kv_dtype=KV_FP8, seed=seed, **kw)
+
+
+def late_chunk(seed: int = 6, **kw) -> Workload:
+    """A late chunk of a long online prompt (64 new tokens on 30,000 cached
+    ones) batched with 8 decode rows at 2,000-token contexts; GQA 64/8, head_dim
+    128.  Chunked prefill (Section 2.1) reaches such chunks for every long
+    prompt; its few query tiles span many keys."""
+    rows = [RowSpec(PREFILL, 30000, 64)] + [RowSpec(DECODE, 2000, 1) for _ in range(8)]
+    return build("late-chunk", rows, {}, 64, 8, 128, seed=seed, **kw)
 
 
 def random_case(seed: int, num_rows: int = 6, num_q_heads: int = 8, num_kv_heads: int = 2,
