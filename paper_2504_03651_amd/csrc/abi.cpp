@@ -372,8 +372,10 @@ int echo_kv_append(const echo_kv_pool_t *pool, const echo_batch_t *batch, const 
     a.n_units = ((int64_t)batch->num_tokens / kBlock + 2 * (int64_t)batch->num_rows) *
                 pool->num_kv_heads;
     // direct form when a padded grid (every row given the most blocks a row
-    // can write) is at most twice the compact bound: no scan, no LDS
-    const int64_t bpr = std::min<int64_t>(batch->max_q_len / kBlock + 2, batch->max_blocks_per_row);
+    // can write: q tokens span at most (q + 14) / 16 + 1 blocks) is at most
+    // twice the compact bound: no scan, no LDS
+    const int64_t bpr =
+        std::min<int64_t>((batch->max_q_len + kBlock - 2) / kBlock + 1, batch->max_blocks_per_row);
     a.blocks_per_row =
         (int64_t)batch->num_rows * bpr * pool->num_kv_heads <= 2 * a.n_units ? (int32_t)bpr : 0;
     hipError_t e = launch_append(a, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3,
