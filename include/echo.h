@@ -164,7 +164,8 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
  * of the workspace; everything below upload_words is the packed plan:
  *   desc      [n_desc][8]   decode work: tok_off, nt | 1 << 16 when other
  *                           waves read the same keys, bt_row, key_begin,
- *                           key_end, part (first partial slot or -1), 0, 0
+ *                           key_end, part (first partial slot or -1), and
+ *                           for nt == 1 the token and its key limit (else -1, 0)
  *   pdesc     [n_pdesc][8]  prefill work: row, tok0, ntok, key_end,
  *                           key_begin, part, kfull (keys every token of the
  *                           tile sees), 0

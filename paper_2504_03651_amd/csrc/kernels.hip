@@ -528,6 +528,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const int key_begin = __builtin_amdgcn_readfirstlane(ip[3]);
     const int key_end = __builtin_amdgcn_readfirstlane(ip[4]);
     const int dpart = __builtin_amdgcn_readfirstlane(ip[5]);
+    const int tok1 = __builtin_amdgcn_readfirstlane(ip[6]);
+    const int klim1 = __builtin_amdgcn_readfirstlane(ip[7]);
     const int nt = shape & 0xFF;
     const int h0 = kvh * a.group + hc * 16;
     const int nh = min(a.heads_per_chunk, a.group - hc * 16);
@@ -539,8 +541,13 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     const bool qvalid = qi < nt;
     int tok = 0, klim = 0;
     if (qvalid) {
-        tok = a.tok_list[tok_off + qi];
-        klim = a.klim[tok];
+        if (nt == 1) {   // single-token slice: token and key limit ride in the descriptor
+            tok = tok1;
+            klim = klim1;
+        } else {
+            tok = a.tok_list[tok_off + qi];
+            klim = a.klim[tok];
+        }
     }
     const int head = h0 + qj;
 

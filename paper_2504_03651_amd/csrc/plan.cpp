@@ -174,7 +174,8 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
                 d.key_begin = kBlock * j;
                 d.key_end = std::min(kBlock * jend, s.key_end);
                 d.part = -1;
-                d.pad0 = d.pad1 = 0;
+                d.tok1 = ntk == 1 ? plan.tok_list[tok_base + k0] : -1;
+                d.klim1 = ntk == 1 ? plan.klim[d.tok1] : 0;
                 if (!direct) {
                     d.part = (int32_t)n_slots;
                     for (int32_t i = 0; i < ntk; ++i) {

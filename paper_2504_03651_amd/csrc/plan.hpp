@@ -36,7 +36,8 @@ struct WorkDesc {      // 32 bytes
     int32_t key_begin; // first key position, a multiple of 16
     int32_t key_end;   // one past the last key position
     int32_t part;      // first partial slot, or -1: write `out` directly
-    int32_t pad0, pad1;
+    int32_t tok1;      // nt == 1: the slice's token (saves the token-list load)
+    int32_t klim1;     // nt == 1: keys visible to that token
 };
 static_assert(sizeof(WorkDesc) == 32, "descriptor layout");
 

@@ -95,9 +95,13 @@ def test_plan_invariants(w):
     ranges = [[] for _ in range(T)]        # (begin, end, part, slice size, index)
     slot_ranges = []
     for d in desc:
-        tok_off, shape, bt_row, kb, ke, part = (int(x) for x in d[:6])
+        tok_off, shape, bt_row, kb, ke, part, tok1, klim1 = (int(x) for x in d[:8])
         nt = shape & 0xFF
-        assert 1 <= nt <= 16 // hpc * max(1, 1) or nt <= 16
+        if nt == 1:
+            assert tok1 == tok_list[tok_off] and klim1 == klim[tok1]
+        else:
+            assert tok1 == -1
+        assert 1 <= nt <= 16 // hpc
         assert 0 <= tok_off and tok_off + nt <= len(tok_list)
         assert 0 <= bt_row < B and b.row_kind[bt_row] == W.DECODE
         assert kb % 16 == 0 and 0 <= kb < ke <= b.seq_lens[bt_row]
