@@ -78,7 +78,6 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     const int32_t hpc = G < kWaveQueries ? G : kWaveQueries;   // heads per chunk
     const int32_t nhc = (G + kWaveQueries - 1) / kWaveQueries; // head chunks
     const int32_t nt_max = kWaveQueries / hpc;                 // tokens per slice
-    const int32_t split = opt.split_blocks > 0 ? opt.split_blocks : 32;
     plan.head_chunks = nhc;
     plan.heads_per_chunk = hpc;
     plan.waves_per_desc = Hkv * nhc;
@@ -128,6 +127,18 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         seg_rows.push_back(r);
         segs.push_back(s);
     }
+
+    // Key ranges are split into pieces of `split` blocks.  Long pieces keep
+    // the partial results and the merge small; on a small decode batch they
+    // would leave most of the GPU idle while a few waves walk long ranges one
+    // latency-bound step after another, so the pieces shrink (to no fewer
+    // than kMinSplitBlocks) until the batch has about kSplitTargetUnits
+    // (piece, KV head, head chunk) units.
+    int64_t seg_blocks = 0;
+    for (const Segment &s : segs) seg_blocks += s.j1 - s.j0;
+    const int32_t split = (int32_t)std::max<int64_t>(
+        std::min<int32_t>(kMinSplitBlocks, std::max(2, opt.split_blocks)),
+        std::min<int64_t>(opt.split_blocks, seg_blocks * Hkv * nhc / kSplitTargetUnits));
 
     // contributions per decode row: sum over its segments of their splits
     std::vector<int32_t> &cnt = plan.cnt, &moff = plan.moff, &cursor = plan.cursor;

@@ -61,6 +61,8 @@ struct PrefillDesc {   // 32 bytes
 static_assert(sizeof(PrefillDesc) == 32, "prefill descriptor layout");
 constexpr int kPrefillTileKeys = 64;      // keys per LDS tile of the prefill kernel
 constexpr int kPrefillMinPieceTiles = 8;  // shortest piece a long key range is cut into
+constexpr int kMinSplitBlocks = 8;        // shortest decode piece on small batches
+constexpr int kSplitTargetUnits = 2048;   // decode units below which pieces shrink
 
 // Wave w of the attention grid handles descriptor w / (Hkv * head_chunks),
 // KV head (w % (Hkv * head_chunks)) / head_chunks and head chunk

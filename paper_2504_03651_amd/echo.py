@@ -248,7 +248,7 @@ def plan_pack(cpool: CPool, cbatch: CBatch, num_q_heads: int):
     lay = CPlanLayout()
     _check(lib().echo_attn_plan_pack(ctypes.byref(cpool), ctypes.byref(cbatch), int(num_q_heads),
                                      ctypes.byref(lay), None, 0), "echo_attn_plan_pack")
-    words = np.zeros(max(int(lay.upload_words), 1), np.int32)
+    words = np.full(max(int(lay.upload_words), 1), -1, np.int32)   # words the packer skips stay -1
     _check(lib().echo_attn_plan_pack(ctypes.byref(cpool), ctypes.byref(cbatch), int(num_q_heads),
                                      ctypes.byref(lay), words.ctypes.data, words.nbytes),
            "echo_attn_plan_pack")

@@ -185,3 +185,18 @@ def test_plan_pack_buffer_too_small():
     rc = L.echo_attn_plan_pack(ctypes.byref(cp), ctypes.byref(cb), w.num_q_heads,
                                ctypes.byref(lay), buf.ctypes.data, buf.nbytes)
     assert rc == echo.ECHO_E_WORKSPACE
+
+
+def test_small_decode_batches_split_finer():
+    # a late prefill chunk next to a few long decode rows: 48-block pieces
+    # would give 24 descriptors; the planner shrinks them (not below 8 blocks)
+    w = W.config(6)
+    lay, words = _decode(w)
+    d = words[lay["off_desc"]:lay["off_desc"] + 8 * lay["n_desc"]].reshape(-1, 8)
+    blocks = (d[:, 4] - d[:, 3] + 15) // 16
+    assert len(d) > 24 and blocks.max() <= 8
+    # a large batch keeps the long pieces
+    w2 = W.config(2)
+    lay2, words2 = _decode(w2)
+    d2 = words2[lay2["off_desc"]:lay2["off_desc"] + 8 * lay2["n_desc"]].reshape(-1, 8)
+    assert ((d2[:, 4] - d2[:, 3] + 15) // 16).max() == 48
