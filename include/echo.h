@@ -52,7 +52,9 @@ typedef enum {
     ECHO_E_ALIAS_WRITE = -3,  /* an append would write a block another row also reads */
     ECHO_E_WORKSPACE = -4,    /* workspace missing or smaller than required */
     ECHO_E_UNSUPPORTED = -5,  /* head_dim, block_size or dtype not supported */
-    ECHO_E_HIP = -6           /* the HIP runtime reported an error */
+    ECHO_E_HIP = -6,          /* the HIP runtime reported an error */
+    ECHO_E_NOSPACE = -7       /* KV block manager: not enough free blocks, or
+                                 the limit for offline sequences (echo_kvm.h) */
 } echo_status_t;
 
 typedef enum { ECHO_KV_BF16 = 0, ECHO_KV_FP8_E4M3 = 1 } echo_kv_dtype_t;

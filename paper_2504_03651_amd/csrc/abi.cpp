@@ -14,10 +14,9 @@
 #include "echo.h"
 #include "kernels.hpp"
 #include "plan.hpp"
+#include "status.hpp"
 
-using namespace echo;
-
-namespace {
+namespace echo {
 
 thread_local std::string g_error;
 
@@ -30,6 +29,14 @@ int fail(int code, const char *fmt, ...) {
     g_error = buf;
     return code;
 }
+
+void clear_error() { g_error.clear(); }
+
+}  // namespace echo
+
+using namespace echo;
+
+namespace {
 
 int hip_fail(hipError_t e, const char *what) {
     return fail(ECHO_E_HIP, "%s: %s", what, hipGetErrorString(e));
@@ -307,6 +314,7 @@ const char *echo_status_string(int status) {
         case ECHO_E_WORKSPACE: return "ECHO_E_WORKSPACE";
         case ECHO_E_UNSUPPORTED: return "ECHO_E_UNSUPPORTED";
         case ECHO_E_HIP: return "ECHO_E_HIP";
+        case ECHO_E_NOSPACE: return "ECHO_E_NOSPACE";
         default: return "ECHO_E_UNKNOWN";
     }
 }

@@ -22,6 +22,7 @@ ECHO_E_ALIAS_WRITE = -3
 ECHO_E_WORKSPACE = -4
 ECHO_E_UNSUPPORTED = -5
 ECHO_E_HIP = -6
+ECHO_E_NOSPACE = -7
 KV_BF16 = 0
 KV_FP8_E4M3 = 1
 

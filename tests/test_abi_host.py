@@ -16,17 +16,20 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def test_library_exports_every_declared_symbol():
-    header = open(os.path.join(ROOT, "include", "echo.h")).read()
-    declared = set(re.findall(r"\b(echo_[a-z0-9_]+)\s*\(", header))
-    assert declared >= set(echo.SYMBOLS)
+    from paper_2504_03651_amd import kvm
     lib = ctypes.CDLL(echo.LIB_PATH)
-    for name in declared:
-        assert hasattr(lib, name), name
+    for hdr, bound in (("echo.h", echo.SYMBOLS), ("echo_kvm.h", kvm.SYMBOLS)):
+        header = open(os.path.join(ROOT, "include", hdr)).read()
+        declared = set(re.findall(r"\b(echo_[a-z0-9_]+)\s*\(", header))
+        assert declared >= set(bound), hdr
+        assert declared, hdr
+        for name in declared:
+            assert hasattr(lib, name), name
 
 
 def test_status_strings():
     for code, name in [(0, "ECHO_OK"), (-1, "ECHO_E_INVALID"), (-3, "ECHO_E_ALIAS_WRITE"),
-                       (-6, "ECHO_E_HIP")]:
+                       (-6, "ECHO_E_HIP"), (-7, "ECHO_E_NOSPACE")]:
         assert echo.status_string(code) == name
 
 

@@ -1,0 +1,341 @@
+"""Task-aware KV block manager (include/echo_kvm.h) against its plain oracle.
+
+Pins: the eviction order of Section 4.2's priority list (running online
+blocks never; then offline rc = 0, finished online, rc = 1, rc = 2), least
+recently used first within a priority, prefix reuse of Section 6 (automatic
+prefix caching), the threshold that keeps offline tasks from taking the room
+left for online bursts, and copy-on-write.  The expected sequences are written
+out by hand from those rules and checked on both the library and the oracle.
+Parity: seeded random streams of operations drive both and compare every
+return value, block table, eviction, copy pair, block record and counter.
+"""
+import numpy as np
+import pytest
+
+from oracle.kvm_oracle import KVMOracle
+from paper_2504_03651_amd import kvm
+
+ONLINE, OFFLINE = kvm.ONLINE, kvm.OFFLINE
+NOSPACE = -7
+
+
+class Lib:
+    """The library behind the oracle's interface (status codes, plain lists)."""
+
+    def __init__(self, nb, limit=None):
+        self.m = kvm.KVManager(nb, limit)
+        self.nb = nb
+
+    def register_offline(self, req, toks):
+        return self.m.register_offline(req, toks, check=False)[0]
+
+    def unregister_offline(self, req):
+        return self.m.unregister_offline(req, check=False)[0]
+
+    def start(self, seq, task, toks):
+        return self.m.start(seq, task, toks, check=False)
+
+    def append(self, seq, toks):
+        return self.m.append(seq, toks, check=False)[0]
+
+    def fork(self, p, c):
+        return self.m.fork(p, c, check=False)[0]
+
+    def finish(self, seq):
+        return self.m.finish(seq, check=False)[0]
+
+    def tick(self):
+        self.m.tick()
+        return 0
+
+    def block_tables(self, seqs, mbr):
+        code, out = self.m.block_tables(seqs, mbr, check=False)
+        if code:
+            return code, None
+        bt, sl = out
+        return 0, (bt.tolist(), sl.tolist())
+
+    def take_copies(self):
+        return [tuple(p) for p in self.m.take_copies().tolist()]
+
+    def take_evictions(self):
+        return self.m.take_evictions()
+
+    def block_info(self, b):
+        return self.m.block_info(b)
+
+    def stats(self):
+        return self.m.stats()
+
+
+IMPLS = [pytest.param(Lib, id="library"), pytest.param(KVMOracle, id="oracle")]
+
+
+def toks(tag, n):
+    """n distinct tokens of a family `tag` (same tag, same prefix)."""
+    return [tag * 1000 + i for i in range(n)]
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_eviction_follows_the_priority_list(Impl):
+    m = Impl(6)
+    # block 0: finished offline task, rc 0 (priority 0), last access t=0
+    assert m.start(10, OFFLINE, toks(1, 16)) == (0, 0)
+    assert m.finish(10) == 0
+    m.tick()
+    # block 1: finished online task (priority 1/2), t=1
+    assert m.start(11, ONLINE, toks(2, 16))[0] == 0
+    assert m.finish(11) == 0
+    m.tick()
+    # block 2: prefix of one registered offline prompt (rc 1), t=2
+    assert m.register_offline(100, toks(3, 40)) == 0
+    assert m.start(12, OFFLINE, toks(3, 16))[0] == 0
+    assert m.finish(12) == 0
+    m.tick()
+    # block 3: prefix of two registered offline prompts (rc 2), t=3
+    assert m.register_offline(101, toks(4, 16) + [7] * 20) == 0
+    assert m.register_offline(102, toks(4, 16) + [8] * 30) == 0
+    assert m.start(13, OFFLINE, toks(4, 16))[0] == 0
+    assert m.finish(13) == 0
+    m.tick()
+    # block 4: finished offline task, rc 0, later than block 0 (t=4)
+    assert m.start(14, OFFLINE, toks(5, 16))[0] == 0
+    assert m.finish(14) == 0
+    m.tick()
+    # block 5: a running online task (never evicted)
+    assert m.start(15, ONLINE, toks(6, 10))[0] == 0
+    assert [m.block_info(b)["priority2"] for b in range(6)] == [0, 1, 2, 4, 0, -1]
+    assert [m.block_info(b)["rc"] for b in range(5)] == [0, 0, 1, 2, 0]
+    # a burst of online work needs all five evictable blocks
+    assert m.start(16, ONLINE, toks(7, 80)) == (0, 0)
+    assert m.take_evictions() == [0, 4, 1, 2, 3]
+    code, (bt, sl) = m.block_tables([15, 16], 6)
+    assert code == 0 and bt[0][0] == 5 and sorted(bt[1][:5]) == [0, 1, 2, 3, 4]
+    # nothing is left to evict: the running blocks stay
+    assert m.start(17, ONLINE, toks(8, 1)) == (NOSPACE, -1)
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_lru_within_a_priority_then_deeper_blocks(Impl):
+    m = Impl(5)
+    assert m.start(1, OFFLINE, toks(1, 48))[0] == 0   # blocks 0 1 2
+    m.tick()
+    assert m.start(2, OFFLINE, toks(2, 16))[0] == 0   # block 3
+    m.tick()
+    assert m.finish(2) == 0                             # block 3 released at t=2
+    m.tick()
+    assert m.finish(1) == 0                             # blocks 0-2 released at t=3
+    assert m.start(3, ONLINE, toks(3, 5 * 16 - 1))[0] == 0
+    # block 4 was empty; then oldest first (3), then the t=3 blocks deepest first
+    assert m.take_evictions() == [3, 2, 1, 0]
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_prefix_reuse(Impl):
+    m = Impl(16)
+    a = toks(1, 40)
+    assert m.start(1, OFFLINE, a) == (0, 0)
+    # filled this iteration: not visible before the tick
+    assert m.start(2, OFFLINE, a[:32] + [5] * 3) == (0, 0)
+    m.tick()
+    code, (bt, _) = m.block_tables([1], 4)
+    assert m.start(3, ONLINE, a[:32] + [9] * 10) == (0, 32)
+    code, (bt3, sl3) = m.block_tables([3], 4)
+    assert bt3[0][:2] == bt[0][:2] and bt3[0][2] not in bt[0] and sl3 == [42]
+    assert m.block_info(bt[0][0])["holders"] == 2
+    # a prompt that is cached whole still computes its last block
+    assert m.start(4, ONLINE, a[:32]) == (0, 16)
+    # after its sequences finish the prefix stays cached and is found again
+    for s in (1, 2, 3, 4):
+        assert m.finish(s) == 0
+    assert m.block_info(bt[0][0])["state"] == kvm.CACHED
+    assert m.start(5, OFFLINE, a + [1]) == (0, 32)
+    assert m.stats()["hits_tokens"] == 32 + 16 + 32
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_reference_counts_follow_registration(Impl):
+    m = Impl(8)
+    p = toks(1, 32)
+    assert m.register_offline(7, p + [3]) == 0
+    assert m.register_offline(7, p) == -1          # twice
+    assert m.start(1, OFFLINE, p + [4])[0] == 0
+    m.tick()
+    assert m.finish(1) == 0
+    code, _ = m.block_tables([], 1)
+    infos = [m.block_info(b) for b in range(3)]
+    assert [i["rc"] for i in infos] == [1, 1, 0] and [i["state"] for i in infos] == [2, 2, 0]
+    assert [i["priority2"] for i in infos[:2]] == [2, 2]
+    assert m.register_offline(8, p[:16]) == 0
+    assert [m.block_info(b)["priority2"] for b in range(2)] == [4, 2]
+    assert m.unregister_offline(7) == 0 and m.unregister_offline(8) == 0
+    assert [m.block_info(b)["priority2"] for b in range(2)] == [0, 0]
+    assert m.unregister_offline(8) == -1
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_offline_limit_leaves_room_for_online(Impl):
+    m = Impl(8, 4)
+    assert m.start(1, OFFLINE, toks(1, 5 * 16)) == (NOSPACE, -1)
+    assert m.stats()["held"] == 0                     # nothing changed
+    assert m.start(2, OFFLINE, toks(2, 4 * 16))[0] == 0
+    assert m.append(2, [1]) == NOSPACE                # a fifth offline block
+    assert m.start(3, ONLINE, toks(3, 3 * 16))[0] == 0
+    assert m.append(3, [1]) == 0                      # online: up to the pool
+    assert m.stats()["held"] == 8
+    assert m.start(4, ONLINE, [1]) == (NOSPACE, -1)
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_copy_on_write_after_fork(Impl):
+    m = Impl(8)
+    assert m.start(1, ONLINE, toks(1, 20))[0] == 0    # blocks 0 (full), 1 (4 tokens)
+    assert m.fork(1, 2) == 0
+    assert m.fork(1, 2) == -1
+    assert m.append(2, [42]) == 0                     # shared partial block: copy first
+    assert m.take_copies() == [(1, 2)]
+    code, (bt, sl) = m.block_tables([1, 2], 3)
+    assert bt == [[0, 1, -1], [0, 2, -1]] and sl == [20, 21]
+    assert m.append(1, [43]) == 0                     # now private: no copy
+    assert m.take_copies() == []
+    assert m.block_info(0)["holders"] == 2
+    assert m.block_tables([1], 1)[0] == -2            # more blocks than the row holds
+    assert m.block_tables([9], 3)[0] == -1            # not running
+
+
+def _state(m, nb):
+    return [m.block_info(b) for b in range(nb)], m.stats()
+
+
+@pytest.mark.parametrize("seed", range(6))
+def test_random_streams_match_the_oracle(seed):
+    rng = np.random.default_rng(seed)
+    nb = int(rng.integers(20, 64))
+    limit = int(rng.integers(nb // 2, nb + 1))
+    lib, ora = Lib(nb, limit), KVMOracle(nb, limit)
+    families = [list(rng.integers(0, 50, size=int(rng.integers(16, 70)))) for _ in range(6)]
+    running, next_seq, registered, next_req = [], 0, [], 0
+
+    def both(name, *args):
+        a, b = getattr(lib, name)(*args), getattr(ora, name)(*args)
+        assert a == b, (name, args, a, b)
+        return a
+
+    for step in range(600):
+        op = rng.random()
+        if op < 0.25 or not running:
+            fam = families[int(rng.integers(len(families)))]
+            cut = int(rng.integers(1, len(fam) + 1))
+            tail = list(rng.integers(0, 50, size=int(rng.integers(0, 30))))
+            task = int(rng.integers(2))
+            r = both("start", next_seq, task, fam[:cut] + tail)
+            if r[0] == 0:
+                running.append(next_seq)
+            next_seq += 1
+        elif op < 0.55:
+            s = running[int(rng.integers(len(running)))]
+            both("append", s, list(rng.integers(0, 50, size=int(rng.integers(1, 20)))))
+        elif op < 0.62:
+            s = running[int(rng.integers(len(running)))]
+            if both("fork", s, next_seq) == 0:
+                running.append(next_seq)
+            next_seq += 1
+        elif op < 0.77:
+            s = running.pop(int(rng.integers(len(running))))
+            both("finish", s)
+        elif op < 0.85:
+            fam = families[int(rng.integers(len(families)))]
+            both("register_offline", next_req, fam[:int(rng.integers(0, len(fam) + 1))])
+            registered.append(next_req)
+            next_req += 1
+        elif op < 0.9 and registered:
+            both("unregister_offline", registered.pop(int(rng.integers(len(registered)))))
+        else:
+            both("tick")
+        assert lib.take_evictions() == ora.take_evictions()
+        assert lib.take_copies() == ora.take_copies()
+        if running:
+            both("block_tables", running, 40)
+        if step % 10 == 0:
+            assert _state(lib, nb) == _state(ora, nb)
+    assert _state(lib, nb) == _state(ora, nb)
+    assert ora.stats()["evictions"] > 0   # the stream did exercise eviction
+
+
+class _OnlineLowest(KVMOracle):      # finished online blocks ranked below offline ones
+    def _priority2(self, b):
+        p = super()._priority2(b)
+        return {0: 1, 1: 0}.get(p, p)
+
+
+class _MostRecentFirst(KVMOracle):   # LRU reversed
+    def _take(self):
+        for x in self.blocks:
+            x["lat"] = -x["lat"]
+        try:
+            return super()._take()
+        finally:
+            for x in self.blocks:
+                x["lat"] = -x["lat"]
+
+
+class _RcIgnored(KVMOracle):         # reference counts left out of the priority
+    def _rc(self, b):
+        return 0
+
+
+class _ShallowFirst(KVMOracle):      # equal times: shallower block first
+    def _take(self):
+        for x in self.blocks:
+            x["depth"] = -x["depth"]
+        try:
+            return super()._take()
+        finally:
+            for x in self.blocks:
+                x["depth"] = -x["depth"]
+
+
+class _NoWholeHitRule(KVMOracle):    # a fully cached prompt reuses every block
+    def start(self, seq, task, tokens):
+        code, c = super().start(seq, task, tokens)
+        return code, c + 16 if code == 0 and c and c + 16 == len(tokens) else c
+
+
+@pytest.mark.parametrize("Mutant", [_OnlineLowest, _MostRecentFirst, _RcIgnored, _ShallowFirst,
+                                    _NoWholeHitRule])
+def test_pins_catch_planted_oracle_mistakes(Mutant):
+    pins = [test_eviction_follows_the_priority_list, test_lru_within_a_priority_then_deeper_blocks,
+            test_prefix_reuse, test_reference_counts_follow_registration]
+    caught = 0
+    for pin in pins:
+        try:
+            pin(Mutant)
+        except AssertionError:
+            caught += 1
+    assert caught >= 1, f"{Mutant.__name__} passes every pin"
+
+
+def test_serving_loop_batches_pass_the_iteration_checks():
+    """Batches built from the manager are valid inputs of echo_kv_append /
+    echo_attn_mixed (appends only into blocks no other row reads, ids in
+    range), and the oracle accepts them; the loop exercises prefix hits,
+    copy-on-write and eviction."""
+    import oracle
+    from paper_2504_03651_amd import echo
+    from tests import kvm_serving
+    hits = copies = evictions = 0
+    for seed in range(3):
+        pool = None
+        for w in kvm_serving.iterations(seed):
+            cp, cb, _keep = echo.host_structs(w)
+            assert echo.validate(cp, cb, True) == echo.ECHO_OK, echo.last_error()
+            assert echo.validate(cp, cb, False) == echo.ECHO_OK, echo.last_error()
+            if pool is None:
+                pool = oracle.Pool(w.num_blocks, w.num_kv_heads, w.head_dim, False)
+            if len(w.cow_pairs):
+                oracle.block_copy(pool, w.cow_pairs)
+            oracle.kv_append(pool, w.batch, w.k_new, w.v_new)
+            copies += len(w.cow_pairs)
+            evictions += len(w.evicted)
+            hits = w.stats["hits_tokens"]
+    assert hits > 0 and copies > 0 and evictions > 0, (hits, copies, evictions)
