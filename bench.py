@@ -56,6 +56,9 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-pairs", type=int, default=1024)
+    ap.add_argument("--layer", action="store_true",
+                    help="time a whole LLaMA-3.1-8B-shaped decoder layer around the iteration "
+                         "(configs 3 and 5: GQA 32/8, head_dim 128) instead")
     return ap.parse_args()
 
 
@@ -151,8 +154,65 @@ def copy_benchmark(it, w, n_pairs, reps=5):
     return {"pairs": n, "ms": round(ms, 4), "bytes": moved, "GBps": round(moved / ms / 1e6, 1)}
 
 
+def layer_bench(args):
+    """One decoder layer (RMSNorm, QKV GEMM, RoPE, append, attention, O GEMM,
+    RMSNorm, gate/up GEMM, SiLU, down GEMM) at LLaMA-3.1-8B shapes with random
+    weights, on a configuration's batch: the attention's share of a layer step."""
+    import torch
+    from paper_2504_03651_amd import echo, layer
+    from paper_2504_03651_amd import workload as W
+    from paper_2504_03651_amd.session import Iteration
+    cfg = args.config if args.config in (3, 5) else 3
+    w = W.config(cfg)
+    H, I = 4096, 14336
+    lw = W.layer_weights(1, H, w.num_q_heads, w.num_kv_heads, w.head_dim, I)
+    it = Iteration(w)
+    L = layer.Layer(lw)
+    T = w.batch.num_tokens
+    x = torch.from_numpy(W.layer_hidden(2, T, H).view(np.int16)).cuda()
+    hid = x.clone()
+    ws = torch.empty(L.workspace_bytes(it.pool, it.batch), dtype=torch.uint8, device="cuda")
+    for _ in range(args.warmup):
+        hid.copy_(x)
+        L.forward(it.pool, it.batch, hid, ws)
+    torch.cuda.synchronize()
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+    ev[0].record()
+    for _ in range(args.steps):
+        L.forward(it.pool, it.batch, hid, ws)
+    ev[1].record()
+    torch.cuda.synchronize()
+    ms = ev[0].elapsed_time(ev[1]) / args.steps
+    echo.profile(True)
+    stages = []
+    for _ in range(args.steps):
+        L.forward(it.pool, it.batch, hid, ws)
+        stages.append(layer.timing())
+    echo.profile(False)
+    st = {k: float(np.median([s[k] for s in stages])) for k in stages[0]}
+    tot = sum(st.values())
+    qd, kd = w.num_q_heads * w.head_dim, w.num_kv_heads * w.head_dim
+    gemm_flops = 2.0 * T * (H * (qd + 2 * kd) + qd * H + H * 2 * I + I * H)
+    gemm_ms = st["qkv_ms"] + st["o_ms"] + st["mlp_ms"]
+    out = {"metric": "decoder-layer step tokens/s (LLaMA-3.1-8B-shaped layer around the mixed "
+                     "iteration)", "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s",
+           "n_gpus": 1, "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms, 4),
+           "higher_is_better": True, "dtype": "bf16", "data": "synthetic, random weights",
+           "config": {"workload": f"cfg{cfg}: {DESCRIPTIONS[cfg]}", "hidden": H,
+                      "intermediate": I, "q_heads": w.num_q_heads, "kv_heads": w.num_kv_heads,
+                      "head_dim": w.head_dim, "tokens": T},
+           "stages_ms": {k: round(v, 4) for k, v in st.items()},
+           "attention_share": round((st["attention_ms"] + st["append_ms"]) / tot, 3),
+           "gemm_tflops": round(gemm_flops / (gemm_ms * 1e-3) / 1e12, 1),
+           "gemm_frac_bf16_peak": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 3)}
+    print(json.dumps(out), flush=True)
+    return 0
+
+
 def main():
     args = parse()
+    if args.layer and args.gpus == 1:
+        return layer_bench(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the hot path "
               "shards by KV head or by prefix group with no exchange, but this build runs on a "

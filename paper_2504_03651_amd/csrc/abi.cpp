@@ -241,6 +241,12 @@ struct Profile {
 };
 thread_local Profile g_prof;
 
+}  // namespace
+
+bool echo::profile_enabled() { return g_prof.on; }
+
+namespace {
+
 int profile_events(hipEvent_t **out) {
     *out = nullptr;
     if (!g_prof.on) return ECHO_OK;

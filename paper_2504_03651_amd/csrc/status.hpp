@@ -7,5 +7,7 @@ namespace echo {
 int fail(int code, const char *fmt, ...);
 // Clears the calling thread's detail (every entry point starts with it).
 void clear_error();
+// Whether echo_profile(1) is on for the calling thread.
+bool profile_enabled();
 
 }  // namespace echo

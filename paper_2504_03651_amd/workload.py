@@ -417,3 +417,55 @@ def random_case(seed: int, num_rows: int = 6, num_q_heads: int = 8, num_kv_heads
     groups = {k: 16 * int(g.integers(1, max(2, max_ctx // 16))) for k in range(n_groups)}
     return build(f"random-{seed}", rows, groups, num_q_heads, num_kv_heads, head_dim,
                  kv_dtype=kv_dtype, seed=seed, **kw)
+
+
+# --------------------------------------------------------------------------
+# decoder-layer inputs (random weights of a LLaMA-style layer)
+
+
+def _scaled_bf16(seed: int, stream: int, n: int, scale: float, shift: float = 0.0) -> np.ndarray:
+    """n draws of fp32 shift + scale * N(0,1), rounded to nearest-even bf16."""
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, stream])))
+    x = (np.float32(shift) + np.float32(scale) * g.standard_normal(n, dtype=np.float32))
+    b = x.astype(np.float32).view(np.uint32)
+    b = b + np.uint32(0x7FFF) + ((b >> np.uint32(16)) & np.uint32(1))
+    return (b >> np.uint32(16)).astype(np.uint16)
+
+
+@dataclass
+class LayerWeights:
+    hidden: int
+    num_q_heads: int
+    num_kv_heads: int
+    head_dim: int
+    intermediate: int
+    rope_theta: float
+    rms_eps: float
+    attn_norm: np.ndarray   # [H] bf16 bits
+    w_qkv: np.ndarray       # [(Hq + 2 Hkv) D][H]
+    w_o: np.ndarray         # [H][Hq D]
+    mlp_norm: np.ndarray    # [H]
+    w_gate_up: np.ndarray   # [2 I][H] (gate rows, then up rows)
+    w_down: np.ndarray      # [H][I]
+
+
+def layer_weights(seed: int, hidden: int, num_q_heads: int, num_kv_heads: int, head_dim: int,
+                  intermediate: int, rope_theta: float = 500000.0,
+                  rms_eps: float = 1e-5) -> LayerWeights:
+    """Random weights: linear layers N(0, 1/fan_in), norms 1 + N(0, 0.1^2)."""
+    H, I = hidden, intermediate
+    qkv = (num_q_heads + 2 * num_kv_heads) * head_dim
+    qd = num_q_heads * head_dim
+    return LayerWeights(
+        hidden, num_q_heads, num_kv_heads, head_dim, intermediate, rope_theta, rms_eps,
+        _scaled_bf16(seed, 40, H, 0.1, 1.0),
+        _scaled_bf16(seed, 41, qkv * H, 1.0 / math.sqrt(H)).reshape(qkv, H),
+        _scaled_bf16(seed, 42, H * qd, 1.0 / math.sqrt(qd)).reshape(H, qd),
+        _scaled_bf16(seed, 43, H, 0.1, 1.0),
+        _scaled_bf16(seed, 44, 2 * I * H, 1.0 / math.sqrt(H)).reshape(2 * I, H),
+        _scaled_bf16(seed, 45, H * I, 1.0 / math.sqrt(I)).reshape(H, I))
+
+
+def layer_hidden(seed: int, num_tokens: int, hidden: int) -> np.ndarray:
+    """The layer's input activations [T][H]: N(0,1) bf16 bits."""
+    return _scaled_bf16(seed, 46, num_tokens * hidden, 1.0).reshape(num_tokens, hidden)

@@ -16,9 +16,10 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 
 
 def test_library_exports_every_declared_symbol():
-    from paper_2504_03651_amd import kvm
+    from paper_2504_03651_amd import kvm, layer
     lib = ctypes.CDLL(echo.LIB_PATH)
-    for hdr, bound in (("echo.h", echo.SYMBOLS), ("echo_kvm.h", kvm.SYMBOLS)):
+    for hdr, bound in (("echo.h", echo.SYMBOLS), ("echo_kvm.h", kvm.SYMBOLS),
+                       ("echo_layer.h", layer.SYMBOLS)):
         header = open(os.path.join(ROOT, "include", hdr)).read()
         declared = set(re.findall(r"\b(echo_[a-z0-9_]+)\s*\(", header))
         assert declared >= set(bound), hdr
