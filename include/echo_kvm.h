@@ -78,6 +78,14 @@ int echo_kvm_unregister_offline(echo_kvm_t *m, int64_t req);
 int echo_kvm_start(echo_kvm_t *m, int64_t seq, int32_t task, const int32_t *tokens, int32_t n,
                    int32_t *cached_tokens);
 
+/* How many prompt tokens echo_kvm_start would find cached for tokens[0..n)
+ * (n >= 1), in *cached_tokens, without changing anything. */
+int echo_kvm_probe(const echo_kvm_t *m, const int32_t *tokens, int32_t n, int32_t *cached_tokens);
+
+/* Moves the threshold (0..num_blocks): later offline starts and appends may
+ * not raise the held blocks above it; blocks already held stay. */
+int echo_kvm_set_offline_limit(echo_kvm_t *m, int32_t offline_limit);
+
 /* Appends tokens[0..n) (n >= 1) to running sequence `seq`.  When its last
  * block is partial and shared (after echo_kvm_fork), the block is copied into
  * a new private one first and the pair is queued for echo_kvm_take_copies. */
@@ -126,6 +134,7 @@ typedef struct {
     int64_t now;                  /* clock */
     int64_t hits_tokens;          /* prompt tokens served from the cache so far */
     int64_t evictions;            /* blocks evicted so far */
+    int32_t cached_reusable;      /* cached blocks with rc > 0 (evicting them costs recompute) */
 } echo_kvm_stats_t;
 
 int echo_kvm_stats(const echo_kvm_t *m, echo_kvm_stats_t *stats);

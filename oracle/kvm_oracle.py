@@ -157,6 +157,26 @@ class KVMOracle:
         self.hits_tokens += BS * len(hits)
         return OK, BS * len(hits)
 
+    def probe(self, tokens):
+        toks = tuple(int(t) for t in tokens)
+        n = len(toks)
+        if n < 1:
+            return E_INVALID, -1
+        hits = 0
+        for j in range(n // BS):
+            if toks[:(j + 1) * BS] not in self.cache:
+                break
+            hits += 1
+        if hits == n // BS and n % BS == 0 and hits:
+            hits -= 1
+        return OK, BS * hits
+
+    def set_offline_limit(self, limit):
+        if not 0 <= limit <= self.nb:
+            return E_INVALID
+        self.limit = limit
+        return OK
+
     def append(self, seq, tokens):
         toks = [int(t) for t in tokens]
         if seq not in self.seqs or len(toks) < 1:
@@ -258,4 +278,6 @@ class KVMOracle:
         return dict(empty=sum(1 for x in self.blocks if x["state"] == EMPTY), held=self._held(),
                     cached=sum(1 for x in self.blocks if x["state"] == CACHED),
                     running=len(self.seqs), now=self.now, hits_tokens=self.hits_tokens,
-                    evictions=self.n_evictions)
+                    evictions=self.n_evictions,
+                    cached_reusable=sum(1 for b, x in enumerate(self.blocks)
+                                        if x["state"] == CACHED and self._rc(b) > 0))

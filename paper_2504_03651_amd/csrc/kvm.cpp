@@ -101,19 +101,24 @@ struct echo_kvm {
         if (r > 0) return 2 * r;
         return b.task == ECHO_TASK_ONLINE ? 1 : 0;
     }
+    int32_t cached_reusable = 0;   // cached blocks with rc > 0
     void to_free(int32_t id) {
         Block &b = blk[id];
         b.state = kCached;
         b.key = FreeKey{prio2(b), b.lat, -b.depth, id};
         freetab.insert(b.key);
+        cached_reusable += b.key.p2 >= 2;
     }
-    void from_free(int32_t id) { freetab.erase(blk[id].key); }
+    void from_free(int32_t id) {
+        freetab.erase(blk[id].key);
+        cached_reusable -= blk[id].key.p2 >= 2;
+    }
     void rekey(uint64_t h) {
         auto it = cache.find(h);
         if (it == cache.end()) return;
         Block &b = blk[it->second];
         if (b.state != kCached) return;
-        freetab.erase(b.key);
+        from_free(it->second);
         to_free(it->second);
     }
     void reset(Block &b) { b = Block{}; }
@@ -124,9 +129,8 @@ struct echo_kvm {
             id = *empty.begin();
             empty.erase(empty.begin());
         } else {
-            const FreeKey k = *freetab.begin();
-            freetab.erase(freetab.begin());
-            id = k.id;
+            id = freetab.begin()->id;
+            from_free(id);
             Block &b = blk[id];
             auto it = cache.find(b.hash);
             if (it != cache.end() && it->second == id) cache.erase(it);
@@ -299,6 +303,34 @@ int echo_kvm_start(echo_kvm_t *m, int64_t seq, int32_t task, const int32_t *toke
     return ECHO_OK;
 }
 
+int echo_kvm_probe(const echo_kvm_t *m, const int32_t *tokens, int32_t n, int32_t *cached_tokens) {
+    echo::clear_error();
+    if (!m || !cached_tokens) return fail(ECHO_E_INVALID, "manager or cached_tokens is NULL");
+    int rc = check_tokens(tokens, n, 1);
+    if (rc) return rc;
+    const int32_t nfull = n / kTok;
+    int32_t hits = 0;
+    uint64_t parent = 0;
+    for (int32_t j = 0; j < nfull; ++j) {
+        const uint64_t h = chain_hash(parent, tokens + (size_t)j * kTok);
+        if (m->lookup(parent, h, tokens + (size_t)j * kTok) < 0) break;
+        ++hits;
+        parent = h;
+    }
+    if (hits == nfull && n % kTok == 0 && hits > 0) --hits;
+    *cached_tokens = hits * kTok;
+    return ECHO_OK;
+}
+
+int echo_kvm_set_offline_limit(echo_kvm_t *m, int32_t offline_limit) {
+    echo::clear_error();
+    if (!m) return fail(ECHO_E_INVALID, "manager is NULL");
+    if (offline_limit < 0 || offline_limit > m->nb)
+        return fail(ECHO_E_INVALID, "offline_limit %d of %d blocks", offline_limit, m->nb);
+    m->limit = offline_limit;
+    return ECHO_OK;
+}
+
 int echo_kvm_append(echo_kvm_t *m, int64_t seq, const int32_t *tokens, int32_t n) {
     echo::clear_error();
     if (!m) return fail(ECHO_E_INVALID, "manager is NULL");
@@ -468,6 +500,7 @@ int echo_kvm_stats(const echo_kvm_t *m, echo_kvm_stats_t *st) {
     st->now = m->now;
     st->hits_tokens = m->hits_tokens;
     st->evictions = m->evictions;
+    st->cached_reusable = m->cached_reusable;
     return ECHO_OK;
 }
 

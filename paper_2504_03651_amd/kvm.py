@@ -16,7 +16,8 @@ from . import echo
 SYMBOLS = ["echo_kvm_create", "echo_kvm_destroy", "echo_kvm_register_offline",
            "echo_kvm_unregister_offline", "echo_kvm_start", "echo_kvm_append", "echo_kvm_fork",
            "echo_kvm_finish", "echo_kvm_tick", "echo_kvm_block_tables", "echo_kvm_take_copies",
-           "echo_kvm_take_evictions", "echo_kvm_block_info", "echo_kvm_stats"]
+           "echo_kvm_take_evictions", "echo_kvm_block_info", "echo_kvm_stats", "echo_kvm_probe",
+           "echo_kvm_set_offline_limit"]
 
 ONLINE, OFFLINE = 0, 1
 EMPTY, HELD, CACHED = 0, 1, 2
@@ -31,7 +32,8 @@ class CBlockInfo(ctypes.Structure):
 class CStats(ctypes.Structure):
     _fields_ = [("empty", ctypes.c_int32), ("held", ctypes.c_int32), ("cached", ctypes.c_int32),
                 ("running", ctypes.c_int32), ("now", ctypes.c_int64),
-                ("hits_tokens", ctypes.c_int64), ("evictions", ctypes.c_int64)]
+                ("hits_tokens", ctypes.c_int64), ("evictions", ctypes.c_int64),
+                ("cached_reusable", ctypes.c_int32)]
 
 
 _bound = False
@@ -57,6 +59,8 @@ def _lib():
         L.echo_kvm_take_evictions.argtypes = [vp, vp, i32, ctypes.POINTER(i32)]
         L.echo_kvm_block_info.argtypes = [vp, i32, ctypes.POINTER(CBlockInfo)]
         L.echo_kvm_stats.argtypes = [vp, ctypes.POINTER(CStats)]
+        L.echo_kvm_probe.argtypes = [vp, vp, i32, ctypes.POINTER(i32)]
+        L.echo_kvm_set_offline_limit.argtypes = [vp, i32]
         for n in SYMBOLS:
             if n != "echo_kvm_destroy":
                 getattr(L, n).restype = ctypes.c_int
@@ -113,6 +117,17 @@ class KVManager:
         c = ctypes.c_int32(-1)
         code = self.L.echo_kvm_start(self.h, int(seq), int(task), p, n, ctypes.byref(c))
         return self._ret(code, "echo_kvm_start", int(c.value), check)
+
+    def probe(self, tokens) -> int:
+        """Prompt tokens a start would find cached (no side effects)."""
+        a, p, n = _tok(tokens)
+        c = ctypes.c_int32(-1)
+        echo._check(self.L.echo_kvm_probe(self.h, p, n, ctypes.byref(c)), "echo_kvm_probe")
+        return int(c.value)
+
+    def set_offline_limit(self, limit: int):
+        echo._check(self.L.echo_kvm_set_offline_limit(self.h, int(limit)),
+                    "echo_kvm_set_offline_limit")
 
     def append(self, seq: int, tokens, check: bool = True):
         a, p, n = _tok(tokens)

@@ -38,6 +38,19 @@ class Lib:
     def append(self, seq, toks):
         return self.m.append(seq, toks, check=False)[0]
 
+    def probe(self, toks):
+        try:
+            return 0, self.m.probe(toks)
+        except kvm.echo.EchoError as e:
+            return e.code, -1
+
+    def set_offline_limit(self, limit):
+        try:
+            self.m.set_offline_limit(limit)
+            return 0
+        except kvm.echo.EchoError as e:
+            return e.code
+
     def fork(self, p, c):
         return self.m.fork(p, c, check=False)[0]
 
@@ -250,6 +263,11 @@ def test_random_streams_match_the_oracle(seed):
             next_req += 1
         elif op < 0.9 and registered:
             both("unregister_offline", registered.pop(int(rng.integers(len(registered)))))
+        elif op < 0.93:
+            fam = families[int(rng.integers(len(families)))]
+            both("probe", fam[:int(rng.integers(1, len(fam) + 1))])
+        elif op < 0.95:
+            both("set_offline_limit", int(rng.integers(0, nb + 1)))
         else:
             both("tick")
         assert lib.take_evictions() == ora.take_evictions()
@@ -339,3 +357,16 @@ def test_serving_loop_batches_pass_the_iteration_checks():
             evictions += len(w.evicted)
             hits = w.stats["hits_tokens"]
     assert hits > 0 and copies > 0 and evictions > 0, (hits, copies, evictions)
+
+
+@pytest.mark.parametrize("Impl", IMPLS)
+def test_probe_and_limit(Impl):
+    m = Impl(8, 8)
+    a = toks(1, 40)
+    assert m.start(1, OFFLINE, a)[0] == 0
+    m.tick()
+    assert m.probe(a[:35]) == (0, 32) and m.probe(a[:32]) == (0, 16) and m.probe([5]) == (0, 0)
+    assert m.stats()["held"] == 3                     # probing changed nothing
+    assert m.set_offline_limit(3) == 0
+    assert m.append(1, [1] * 9) == NOSPACE            # a fourth held block
+    assert m.set_offline_limit(9) == -1
