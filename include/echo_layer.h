@@ -55,8 +55,10 @@ size_t echo_layer_workspace_bytes(const echo_layer_t *layer, const echo_kv_pool_
                                   const echo_batch_t *batch);
 
 /* One forward step of the layer for the batch's new tokens (see above).  The
- * pool receives the new tokens' K/V.  Validation as in echo.h; ECHO_E_HIP also
- * covers hipBLASLt failures. */
+ * pool receives the new tokens' K/V.  Arguments, pool and batch are validated
+ * before anything is enqueued, as in echo.h; a HIP or hipBLASLt failure
+ * afterwards (ECHO_E_HIP) can leave the stages before it enqueued, with
+ * hidden and the pool then undefined. */
 int echo_layer_forward(const echo_layer_t *layer, const echo_kv_pool_t *pool,
                        const echo_batch_t *batch, void *hidden, void *workspace,
                        size_t workspace_bytes, void *stream);

@@ -18,6 +18,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <atomic>
 #include <stdint.h>
 
 #include "kernels.hpp"
@@ -1306,13 +1307,19 @@ int prefill_max_blocks(int head_dim) {
 
 template <int D, bool FP8>
 static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
-    static bool attr_set = false;
+    // the dynamic-LDS limit, raised once per device (bit d: done on device d;
+    // concurrent first calls both set it, which is harmless)
+    static std::atomic<uint64_t> attr_devices{0};
     const int bytes = PfLds<D>::BYTES + 4 * p.max_blocks;
-    if (!attr_set) {
-        hipError_t e = hipFuncSetAttribute((const void *)prefill_kernel<D, FP8>,
-                                           hipFuncAttributeMaxDynamicSharedMemorySize, kPfLdsLimit);
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    const uint64_t bit = dev >= 0 && dev < 64 ? (1ull << dev) : 0;
+    if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
+        e = hipFuncSetAttribute((const void *)prefill_kernel<D, FP8>,
+                                hipFuncAttributeMaxDynamicSharedMemorySize, kPfLdsLimit);
         if (e != hipSuccess) return e;
-        attr_set = true;
+        attr_devices.fetch_or(bit, std::memory_order_release);
     }
     const dim3 grid((unsigned)(8 * p.per_xcd)), block(kPfThreads);
     hipLaunchKernelGGL((prefill_kernel<D, FP8>), grid, block, bytes, s, p);
