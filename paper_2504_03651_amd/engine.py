@@ -1,0 +1,72 @@
+"""Runs the scheduler simulation's batches on the GPU through the hot path.
+
+An ``AttentionEngine`` owns a device KV pool of the simulator's block count and
+executes each iteration's batch exactly as the simulator's KV block manager
+lays it out: its block tables and sequence lengths become the rows of an
+``echo_kv_append`` + ``echo_attn_mixed`` call (prefill chunks and decode
+tokens, with seeded N(0, 1) bf16 Q/K/V for the new tokens; there is no
+model), so the manager's tables, evictions and prefix hits all reach the
+kernels.  Each call is timed with events on the stream, to set against the
+estimator's prediction for the same batch.
+"""
+from __future__ import annotations
+
+import numpy as np
+
+from . import echo
+from . import workload as W
+
+BS = 16
+
+
+class AttentionEngine:
+    def __init__(self, num_blocks: int, num_q_heads: int = 32, num_kv_heads: int = 8,
+                 head_dim: int = 128, seed: int = 0, device: str = "cuda"):
+        import torch
+        self.torch = torch
+        self.Hq, self.Hkv, self.D = num_q_heads, num_kv_heads, head_dim
+        self.pool = echo.KVPool(num_blocks, num_kv_heads, head_dim, False, device).poison()
+        self.rng = np.random.default_rng(seed)
+        self.device = device
+        self.ws = None
+        self.ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
+        self.calls = 0
+
+    def _bf16(self, shape):
+        x = self.rng.standard_normal(shape, dtype=np.float32)
+        u = x.view(np.uint32)
+        return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+
+    def __call__(self, manager, batch) -> float:
+        """Runs one batch (list of (request, "prefill" | "decode", new tokens))
+        whose KV blocks `manager` already holds; returns the GPU time in ms."""
+        torch = self.torch
+        seqs = [r.seq for r, kind, n in batch]
+        mbr = max(1, max(-(-(r.computed + r.generated + 1) // BS) for r, k, n in batch))
+        while True:
+            code, out = manager.block_tables(seqs, mbr, check=False)
+            if code == 0:
+                break
+            mbr *= 2
+        bt, sl = out
+        q = np.array([n for r, kind, n in batch], np.int32)
+        kind = np.array([W.PREFILL if k == "prefill" else W.DECODE for r, k, n in batch], np.uint8)
+        b = W.Batch(bt, sl, np.concatenate([[0], np.cumsum(q)]).astype(np.int32), kind)
+        T = int(q.sum())
+        dev = lambda a: torch.from_numpy(a.view(np.int16)).to(self.device)
+        qd = dev(self._bf16((T, self.Hq, self.D)))
+        kd = dev(self._bf16((T, self.Hkv, self.D)))
+        vd = dev(self._bf16((T, self.Hkv, self.D)))
+        db = echo.DeviceBatch(b, self.device)
+        n = echo.workspace_bytes(self.pool, db, self.Hq)
+        if self.ws is None or self.ws.numel() < n:
+            self.ws = torch.empty(max(n, 1 << 20), dtype=torch.uint8, device=self.device)
+        out_t = torch.empty((T, self.Hq, self.D), dtype=torch.float32, device=self.device)
+        self.ev[0].record()
+        echo.kv_append(self.pool, db, kd, vd)
+        echo.attn_mixed(self.pool, db, qd, self.Hq, 1.0 / float(np.sqrt(self.D)), out_t, self.ws)
+        self.ev[1].record()
+        torch.cuda.synchronize()
+        self.calls += 1
+        self.last_out = out_t
+        return float(self.ev[0].elapsed_time(self.ev[1]))
