@@ -119,6 +119,7 @@ int echo_kv_append(const echo_kv_pool_t *pool, const echo_batch_t *batch, const 
  * iteration first: attention reads the new tokens from the pool.  Blocks
  * that several decode rows share are read once per KV head for all of them.
  * q: bf16 [T][num_q_heads][head_dim]; out: fp32 [T][num_q_heads][head_dim].
+ * sm_scale must be positive and finite (ECHO_E_INVALID otherwise).
  * workspace: device scratch of at least echo_attn_workspace_bytes() bytes,
  * 256-byte aligned, not used concurrently by another call.  Host mirrors
  * are required (ECHO_E_INVALID without them). */

@@ -4,6 +4,7 @@
 
 #include <algorithm>
 #include <atomic>
+#include <cmath>
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
@@ -531,6 +532,8 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     if (rc) return rc;
     if (batch->num_rows == 0) return ECHO_OK;
     if (!q || !out) return fail(ECHO_E_INVALID, "q / out is NULL");
+    if (!(sm_scale > 0.f) || !std::isfinite(sm_scale))
+        return fail(ECHO_E_INVALID, "sm_scale must be positive and finite");
     const size_t need = (size_t)plan.layout.total_words * 4;
     if (!workspace || workspace_bytes < need)
         return fail(ECHO_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);

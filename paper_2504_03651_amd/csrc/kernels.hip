@@ -66,14 +66,22 @@ __device__ __forceinline__ uint32_t f32_to_e4m3(float y) {
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
+// v_max_f32 as such: fmaxf adds a canonicalising max of each operand the
+// compiler cannot prove canonical (lane-swap results are not), two extra VALU
+// ops per call.  Used on attention scores, which are finite or -inf.
+__device__ __forceinline__ float vmax(float a, float b) {
+    float r;
+    asm("v_max_f32 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+    return r;
+}
 // max over lanes l, l^16, l^32, l^48 with VALU lane swaps (no LDS traffic):
 // each swap returns the lane's own value and its partner's, in some order.
 __device__ __forceinline__ float wave_max_xor16_32(float x) {
     typedef uint32_t u2 __attribute__((ext_vector_type(2)));
     const u2 a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+    x = vmax(__uint_as_float(a[0]), __uint_as_float(a[1]));
     const u2 b = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-    return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+    return vmax(__uint_as_float(b[0]), __uint_as_float(b[1]));
 }
 
 // ------------------------------------------------------------------- append
@@ -816,6 +824,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
         for (int i = 0; i < NT; ++i) acc[nn][i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
     float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    // derived from m_run, refreshed when it moves: the exponent offset
+    // (-m_run, 0 while m_run is -inf) and the two lazy-rescale thresholds
+    float m_neg[2] = {0.f, 0.f}, m_hi64[2] = {-INFINITY, -INFINITY}, m_hi8[2] = {-INFINITY, -INFINITY};
     // bf16: the softmax denominator is a P.V product with V = 1 (every row of
     // lacc[nn] holds the column sum), so it sums exactly the rounded weights
     // that P.V uses and costs one MFMA per chunk instead of 16 adds per lane.
@@ -927,7 +938,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // for the tile; it moves at the end of the tile when the tile's max
     // exceeds it by more than 8 (rescaling acc and l), or, before a chunk's
     // exponentials, when a chunk's max exceeds it by more than 64 (rare guard
-    // that also covers the first tile, where m_run is still -inf).
+    // that also covers the first tile, where m_run is still -inf).  Both
+    // tests take any lane whose own scores cross the threshold, which is the
+    // same as the column's maximum crossing it.
     auto qk = [&](const uint8_t *kl, int ch, f32x4_t (&sc)[2][2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -946,7 +959,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
             }
     };
     const float f = FP8 ? 1.f : scale;  // raw score -> log2 units (e4m3 scales first)
-    // scale (e4m3), mask, and the chunk max per query column in log2 units
+    // scale (e4m3), mask, and this lane's max over its 8 scores of each query
+    // column in log2 units (the column's max over its 4 lanes is formed only
+    // on the rare rescale path)
     auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2],
                     float &svc) {
         float sk = scale;
@@ -970,7 +985,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                     sc[t][nn][r] = v;
                     mx = fmaxf(mx, v);
                 }
-            mc[nn] = wave_max_xor16_32(mx) * f;
+            mc[nn] = mx * f;
         }
     };
     auto rescale = [&](const float (&mnew)[2]) {
@@ -982,6 +997,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
             for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha;
             m_run[nn] = mnew[nn];
+            m_neg[nn] = mnew[nn] == -INFINITY ? 0.f : -mnew[nn];
+            m_hi64[nn] = mnew[nn] + 64.f;
+            m_hi8[nn] = mnew[nn] + 8.f;
         }
     };
     // exponentials of one chunk against m_run, packed to bf16.  e4m3: the
@@ -991,12 +1009,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     auto expo = [&](const f32x4_t (&sc)[2][2], float svc, bf16x8_t (&pf)[2], bf16x8_t (&pl)[2]) {
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
-            const float muse = m_run[nn] == -INFINITY ? 0.f : m_run[nn];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
-                    const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, -muse));
+                    const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, m_neg[nn]));
                     if constexpr (FP8) {
                         l_run[nn] += pe;
                         const float x = pe * svc;
@@ -1036,16 +1053,18 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         bf16x8_t p0[2], p1[2], l0[2], l1[2];
         qk(kl, 0, s0);
         prep(buf, kt, 0, masked, s0, m0, sv0);
-        if (__any(m0[0] > m_run[0] + 64.f || m0[1] > m_run[1] + 64.f)) {
-            const float mn[2] = {fmaxf(m_run[0], m0[0]), fmaxf(m_run[1], m0[1])};
+        if (__any(m0[0] > m_hi64[0] || m0[1] > m_hi64[1])) {
+            const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m0[0])),
+                                 fmaxf(m_run[1], wave_max_xor16_32(m0[1]))};
             rescale(mn);
         }
         qk(kl, 1, s1);          // MFMA ...
         expo(s0, sv0, p0, l0);  // ... with the exponentials of chunk 0
         prep(buf, kt, 1, masked, s1, m1, sv1);
-        if (__any(m1[0] > m_run[0] + 64.f || m1[1] > m_run[1] + 64.f)) {
+        if (__any(m1[0] > m_hi64[0] || m1[1] > m_hi64[1])) {
             // chunk 0's probabilities, not yet added, move with the reference
-            const float mn[2] = {fmaxf(m_run[0], m1[0]), fmaxf(m_run[1], m1[1])};
+            const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m1[0])),
+                                 fmaxf(m_run[1], wave_max_xor16_32(m1[1]))};
 #pragma unroll
             for (int nn = 0; nn < 2; ++nn) {
                 const float alpha =
@@ -1067,10 +1086,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         pv(vl, 0, p0, l0);      // MFMA ...
         expo(s1, sv1, p1, l1);  // ... with the exponentials of chunk 1
         pv(vl, 1, p1, l1);
-        const float mt[2] = {fmaxf(m0[0], m1[0]), fmaxf(m0[1], m1[1])};
-        if (__any(mt[0] > m_run[0] + 8.f || mt[1] > m_run[1] + 8.f)) {
-            const float mn[2] = {mt[0] > m_run[0] + 8.f ? mt[0] : m_run[0],
-                                 mt[1] > m_run[1] + 8.f ? mt[1] : m_run[1]};
+        const float mt[2] = {vmax(m0[0], m1[0]), vmax(m0[1], m1[1])};
+        if (__any(mt[0] > m_hi8[0] || mt[1] > m_hi8[1])) {
+            const float mc[2] = {wave_max_xor16_32(mt[0]), wave_max_xor16_32(mt[1])};
+            const float mn[2] = {mc[0] > m_hi8[0] ? mc[0] : m_run[0],
+                                 mc[1] > m_hi8[1] ? mc[1] : m_run[1]};
             rescale(mn);
         }
     };

@@ -120,6 +120,17 @@ def test_attention_without_mirrors_is_rejected_before_any_work():
     assert n == 0 and "host mirrors" in echo.last_error()
 
 
+@pytest.mark.parametrize("scale", [0.0, -0.125, float("nan"), float("inf")])
+def test_attention_rejects_non_positive_scale(scale):
+    # raw scores are reduced to a maximum before scaling, which needs scale > 0
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    fake = ctypes.c_void_p(256)   # never dereferenced: validation fails first
+    rc = echo.lib().echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 4, scale, fake,
+                                    None, 0, None)
+    assert rc == echo.ECHO_E_INVALID and "sm_scale" in echo.last_error()
+
+
 def test_block_copy_pair_rules():
     w = W.config1()
     cp, cb, keep = _structs(w)
