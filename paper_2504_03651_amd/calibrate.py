@@ -24,22 +24,30 @@ import numpy as np
 from . import workload as W
 from .estimator import DecodeModel, Estimator, MixedModel, PrefillModel
 
+# spin before each timed call: long enough to cover the host's planning
+GATE_CYCLES = 1_000_000
+
 
 def _time(w, reps):
+    """GPU time of one iteration (KV append + attention), median over reps.
+    Each repetition starts behind a short spin on the stream, so the host's
+    validation and planning overlap it and the events see device work only."""
     import torch
     from .session import Iteration
     it = Iteration(w)
     for _ in range(2):
         it.append()
         it.attend()
-    s = [torch.cuda.Event(enable_timing=True) for _ in range(reps + 1)]
-    s[0].record()
-    for i in range(reps):
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+          for _ in range(reps)]
+    for e0, e1 in ev:
+        torch.cuda._sleep(GATE_CYCLES)
+        e0.record()
         it.append()
         it.attend()
-        s[i + 1].record()
+        e1.record()
     torch.cuda.synchronize()
-    return float(np.median([s[i].elapsed_time(s[i + 1]) for i in range(reps)]))
+    return float(np.median([e0.elapsed_time(e1) for e0, e1 in ev]))
 
 
 def _w(rows, cfg, seed):
@@ -140,8 +148,8 @@ def markdown(out, command):
     lines = [f"# Estimator calibration ({c['config']['hq']}/{c['config']['hkv']} heads, "
              f"head_dim {c['config']['d']}, {c['config']['dtype']})", "",
              "```", command, "```", "",
-             "Times are one iteration of the library (KV append + attention), median of the "
-             "repetitions, CUDA events on the stream.", "",
+             "Times are the GPU time of one iteration of the library (KV append + attention; "
+             "host planning excluded), median of the repetitions, events on the stream.", "",
              f"* prefill T = max(alpha l^2 + beta l, c): alpha = {p['alpha']:.4g} ms, "
              f"beta = {p['beta']:.4g} ms, c = {p['c']:.4g} ms",
              "* decode T = gamma max(L) + delta mean(L) + eps, per batch size n:", ""]

@@ -6,8 +6,9 @@ lays it out: its block tables and sequence lengths become the rows of an
 ``echo_kv_append`` + ``echo_attn_mixed`` call (prefill chunks and decode
 tokens, with seeded N(0, 1) bf16 Q/K/V for the new tokens; there is no
 model), so the manager's tables, evictions and prefix hits all reach the
-kernels.  Each call is timed with events on the stream, to set against the
-estimator's prediction for the same batch.
+kernels.  The GPU time of each call (host planning excluded) is measured with
+events on the stream, to set against the estimator's prediction for the same
+batch.
 """
 from __future__ import annotations
 
@@ -15,6 +16,7 @@ import numpy as np
 
 from . import echo
 from . import workload as W
+from .calibrate import GATE_CYCLES
 
 BS = 16
 
@@ -31,6 +33,7 @@ class AttentionEngine:
         self.ws = None
         self.ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         self.calls = 0
+        self.gate_cycles = GATE_CYCLES
 
     def _bf16(self, shape):
         x = self.rng.standard_normal(shape, dtype=np.float32)
@@ -49,6 +52,19 @@ class AttentionEngine:
                 break
             mbr *= 2
         bt, sl = out
+        # what the kernel-level estimate needs: each prefill chunk's cached
+        # context and the distinct KV tokens the decode rows read
+        seen = {}
+        for i, (r, k, n) in enumerate(batch):
+            if k == "decode":
+                L = int(sl[i])
+                for j in range(-(-L // BS)):
+                    b = int(bt[i, j])
+                    seen[b] = max(seen.get(b, 0), min(BS, L - BS * j))
+        self.last_shape = dict(
+            prefill=[(n, int(sl[i]) - n) for i, (r, k, n) in enumerate(batch) if k == "prefill"],
+            decode=[int(sl[i]) for i, (r, k, n) in enumerate(batch) if k == "decode"],
+            decode_unique=sum(seen.values()))
         q = np.array([n for r, kind, n in batch], np.int32)
         kind = np.array([W.PREFILL if k == "prefill" else W.DECODE for r, k, n in batch], np.uint8)
         b = W.Batch(bt, sl, np.concatenate([[0], np.cumsum(q)]).astype(np.int32), kind)
@@ -62,6 +78,10 @@ class AttentionEngine:
         if self.ws is None or self.ws.numel() < n:
             self.ws = torch.empty(max(n, 1 << 20), dtype=torch.uint8, device=self.device)
         out_t = torch.empty((T, self.Hq, self.D), dtype=torch.float32, device=self.device)
+        # The events bracket GPU work only: a short spin keeps the stream busy
+        # while the host validates and plans the two calls, so the first event
+        # fires with their kernels already queued behind it.
+        torch.cuda._sleep(self.gate_cycles)
         self.ev[0].record()
         echo.kv_append(self.pool, db, kd, vd)
         echo.attn_mixed(self.pool, db, qd, self.Hq, 1.0 / float(np.sqrt(self.D)), out_t, self.ws)

@@ -164,6 +164,31 @@ class Estimator:
             return tp + td
         return float(self.mixed.predict(tp, td))
 
+    def batch_time_kernel(self, prefill_chunks, decode_lens, decode_unique_tokens=None):
+        """The same forms and coefficients read for this library's kernels
+        instead of an engine that runs prefills one after another and reads
+        every row's KV separately: the prefill chunks of a batch run in one
+        launch, so their work terms add and the floor c applies once; a chunk
+        of n new tokens after ctx cached ones has n ctx + n^2 / 2 (query, key)
+        pairs, which alpha l^2 prices as l^2 / 2 for a whole prompt; decode
+        rows that share prefix blocks read them once, so the mean term takes
+        the distinct KV tokens per row (decode_unique_tokens / n).
+        prefill_chunks: (n, ctx) pairs; decode_lens: the rows' lengths."""
+        p = self.prefill
+        tp = 0.0
+        if len(prefill_chunks):
+            work = sum(p.alpha * (n * n + 2.0 * n * c) + p.beta * n for n, c in prefill_chunks)
+            tp = max(float(work), p.c)
+        td = 0.0
+        if len(decode_lens):
+            L = np.asarray(decode_lens, np.float64)
+            g, d, e = self.decode.coef(len(L))
+            mean = float(L.mean()) if decode_unique_tokens is None else decode_unique_tokens / len(L)
+            td = g * float(L.max()) + d * mean + e
+        if tp == 0.0 or td == 0.0:
+            return tp + td
+        return float(self.mixed.predict(tp, td))
+
     def to_dict(self):
         return {"prefill": asdict(self.prefill), "decode": asdict(self.decode),
                 "mixed": asdict(self.mixed), "config": self.config}

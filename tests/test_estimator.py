@@ -80,3 +80,23 @@ def test_mixed_sum_form():
     td = np.array([0.4, 0.3, 0.2])
     m = MixedModel.fit(tp, td, tp + td - 0.03, form="sum")
     assert m.kappa == pytest.approx(0.03) and m.predict(0.2, 0.1) == pytest.approx(0.27)
+
+
+def test_kernel_reading_of_the_forms():
+    est = Estimator(PrefillModel(1e-6, 1e-3, 0.05),
+                    DecodeModel([8, 32], [1e-4, 2e-4], [1e-3, 3e-3], [0.01, 0.02]),
+                    MixedModel(kappa=0.005, form="sum"))
+    # one whole prompt, no sharing: the paper's forms exactly
+    assert est.batch_time_kernel([(300, 0)], []) == pytest.approx(est.batch_time([300], []))
+    L = [100, 200, 300, 400] * 4
+    assert est.batch_time_kernel([], L, sum(L)) == pytest.approx(est.batch_time([], L))
+    assert est.batch_time_kernel([(300, 0)], L) == pytest.approx(est.batch_time([300], L))
+    # chunks share one launch: the floor is paid once, work terms add
+    assert est.batch_time_kernel([(10, 0), (10, 0)], []) == pytest.approx(0.05)
+    assert est.batch_time([10, 10], []) == pytest.approx(0.10)
+    # a chunk after cached context: n ctx + n^2 / 2 pairs at 2 alpha each
+    assert est.batch_time_kernel([(100, 1000)], []) == pytest.approx(
+        max(1e-6 * (100 * 100 + 2 * 100 * 1000) + 1e-3 * 100, 0.05))
+    # shared prefix blocks read once: the mean term takes distinct tokens per row
+    g, d, e = est.decode.coef(16)
+    assert est.batch_time_kernel([], L, 1000) == pytest.approx(g * 400 + d * 1000 / 16 + e)
