@@ -162,14 +162,16 @@ HostBatch host_batch(const echo_batch_t *b) {
     return h;
 }
 
-PlanOptions plan_options() {
+PlanOptions plan_options(const echo_kv_pool_t *pool) {
     PlanOptions o;
-    static const int split = [] {
+    static const int split = [] {   // override for tuning sweeps
         const char *e = getenv("ECHO_SPLIT_BLOCKS");
         int v = e ? atoi(e) : 0;
-        return v > 0 ? v : 48;
+        return v > 0 ? v : 0;
     }();
-    o.split_blocks = split;
+    const int64_t block_bytes = 2 * (int64_t)kBlock * pool->head_dim *
+                                (pool->dtype == ECHO_KV_FP8_E4M3 ? 1 : 2);
+    o.split_blocks = split > 0 ? split : (int)std::max<int64_t>(1, kSplitBytes / block_bytes);
     // compute units of the current device (256 on MI355X; also the value
     // used by host-only calls made where no device is present)
     static std::atomic<int> cus[64];
@@ -212,7 +214,7 @@ int plan_for(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_
         return ECHO_OK;
     }
     return build_plan(host_batch(batch), pool->num_kv_heads, num_q_heads, pool->head_dim,
-                      plan_options(), plan);
+                      plan_options(pool), plan);
 }
 
 // Pinned host staging for plan uploads: a small ring per device, each slot

@@ -61,6 +61,11 @@ struct PrefillDesc {   // 32 bytes
 static_assert(sizeof(PrefillDesc) == 32, "prefill descriptor layout");
 constexpr int kPrefillTileKeys = 64;      // keys per LDS tile of the prefill kernel
 constexpr int kPrefillMinPieceTiles = 8;  // shortest piece a long key range is cut into
+// Decode key ranges are cut into pieces of about kSplitBytes of K+V per KV
+// head: 48 blocks of bf16 at head_dim 128, 96 of e4m3, whose waves move half
+// the bytes per block (a sweep of 16-128 blocks on the decode-only, mixed and
+// e4m3 batches).
+constexpr int64_t kSplitBytes = 384 * 1024;
 constexpr int kMinSplitBlocks = 8;        // shortest decode piece on small batches
 constexpr int kSplitTargetUnits = 2048;   // decode units below which pieces shrink
 
@@ -105,7 +110,7 @@ struct HostBatch {
 };
 
 struct PlanOptions {
-    int split_blocks = 48;  // key blocks per decode split
+    int split_blocks = 48;  // key blocks per decode split (set from kSplitBytes)
     int num_cus = 256;      // compute units: prefill key ranges are cut into
                             // pieces when workgroups would fill at most half of them
 };

@@ -200,3 +200,8 @@ def test_small_decode_batches_split_finer():
     lay2, words2 = _decode(w2)
     d2 = words2[lay2["off_desc"]:lay2["off_desc"] + 8 * lay2["n_desc"]].reshape(-1, 8)
     assert ((d2[:, 4] - d2[:, 3] + 15) // 16).max() == 48
+    # e4m3 pieces hold as many bytes: twice the blocks
+    w5 = W.config(5)
+    lay5, words5 = _decode(w5)
+    d5 = words5[lay5["off_desc"]:lay5["off_desc"] + 8 * lay5["n_desc"]].reshape(-1, 8)
+    assert ((d5[:, 4] - d5[:, 3] + 15) // 16).max() == 96
