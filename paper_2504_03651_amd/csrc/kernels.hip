@@ -20,13 +20,23 @@
 #include <algorithm>
 #include <atomic>
 #include <stdint.h>
+#include <type_traits>
 
 #include "kernels.hpp"
 
 namespace echo {
 
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
+// P.V products: bf16 (bf16 cache) or fp16 (e4m3 cache) operands, fp32 accumulate
+__device__ __forceinline__ f32x4_t mfma_pv(bf16x8_t a, bf16x8_t b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+__device__ __forceinline__ f32x4_t mfma_pv(f16x8_t a, f16x8_t b, f32x4_t c) {
+    return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
@@ -718,8 +728,8 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 //
 // One workgroup = 8 waves x 32 query vectors (consecutive tokens of one
 // prefill chunk x the query heads of one KV head), one workgroup per CU.
-// K/V tiles of 64 keys live in a 3-stage LDS ring as bf16, shared by the
-// eight waves; bf16 tiles are requested two tiles ahead:
+// K/V tiles of 64 keys live in a 3-stage LDS ring as bf16 (e4m3 caches: V as
+// fp16), shared by the eight waves; bf16 tiles are requested two tiles ahead:
 //   K  [64 keys][D]            16-byte chunk q of row r stored at q ^ kswz(r)
 //   V  [4 blocks][D][16 keys]  (the pool's block layout) with the two 16-byte
 //                              halves of row d swapped when bit 3 of d is set
@@ -728,7 +738,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // lane touches all 64 LDS banks once (and 8-lane reads 32 banks once).
 // bf16 pools are copied global -> LDS directly (global_load_lds_dwordx4, no
 // staging registers); e4m3 pools go through registers and are widened to bf16
-// on the way in.  Tiles of keys at or past the last token's position get
+// on the way in (K), or to fp16 after multiplication by the (block, head)
+// scale (V; K scales multiply the logits instead).  Tiles of keys at or past the last
+// token's position get
 // their V entries zeroed (0 * NaN is NaN for unwritten slots).
 
 constexpr int kPfKeys = 64;
@@ -751,7 +763,7 @@ struct PfLds {
     static constexpr int KBYTES = kPfKeys * 2 * D;   // K region of a stage
     static constexpr int VBYTES = 4 * 16 * D * 2;    // V region of a stage
     static constexpr int STAGE = KBYTES + VBYTES;    // bytes
-    static constexpr int BYTES = kPfStages * STAGE + kPfStages * 8 * 4;  // + 4 bytes per block id
+    static constexpr int BYTES = kPfStages * STAGE + kPfStages * 4 * 4;  // + 4 bytes per block id
 };
 
 // s_waitcnt operand: vmcnt(n) with expcnt and lgkmcnt left free
@@ -765,6 +777,14 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     typedef typename kv::T KT;
     typedef typename kv::VRaw Raw;   // 8 codes (16 or 8 bytes)
     typedef PfLds<D> LD;
+    // P.V operand types.  e4m3: V times its block scale, and P, are fp16 (11
+    // significant bits: the scaled values are not bf16-exact, and bf16's 8
+    // bits would put errors up to 2^-9 |v| on rows with few keys)
+    typedef std::conditional_t<FP8, _Float16, __bf16> PE;
+    typedef std::conditional_t<FP8, f16x8_t, bf16x8_t> PT;
+    // chunk guard of the lazy rescale (log2 units): probabilities stay below
+    // 2^kGuard, inside fp16's range for e4m3
+    constexpr float kGuard = FP8 ? 15.f : 64.f;
     constexpr int NC = D / 32, NT = D / 16;
     constexpr int CHUNKS = D / 8;              // 16-byte chunks per K row
     constexpr int NJ = D / (8 * kPfWaves);     // 1 KiB copies per wave per region per tile
@@ -774,8 +794,8 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
         return D == 128 ? ((r & 3) | ((r >> 1) & 0xC)) : (((r >> 1) & 1) | ((r >> 2) & 6));
     };
     extern __shared__ __align__(16) uint8_t lds[];
-    float *lscale = (float *)(lds + kPfStages * LD::STAGE);  // [stage][k 4 | v 4]
-    int32_t *lids = (int32_t *)(lscale + kPfStages * 8);      // the row's block ids
+    float *lscale = (float *)(lds + kPfStages * LD::STAGE);  // [stage][4]: K scales
+    int32_t *lids = (int32_t *)(lscale + kPfStages * 4);      // the row's block ids
 
     const int P = blockIdx.x;
     const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
@@ -823,18 +843,19 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     for (int nn = 0; nn < 2; ++nn)
 #pragma unroll
         for (int i = 0; i < NT; ++i) acc[nn][i] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
-    float m_run[2] = {-INFINITY, -INFINITY}, l_run[2] = {0.f, 0.f};
+    float m_run[2] = {-INFINITY, -INFINITY};
     // derived from m_run, refreshed when it moves: the exponent offset
     // (-m_run, 0 while m_run is -inf) and the two lazy-rescale thresholds
-    float m_neg[2] = {0.f, 0.f}, m_hi64[2] = {-INFINITY, -INFINITY}, m_hi8[2] = {-INFINITY, -INFINITY};
-    // bf16: the softmax denominator is a P.V product with V = 1 (every row of
+    float m_neg[2] = {0.f, 0.f}, m_hig[2] = {-INFINITY, -INFINITY}, m_hi8[2] = {-INFINITY, -INFINITY};
+    // The softmax denominator is a P.V product with V = 1 (every row of
     // lacc[nn] holds the column sum), so it sums exactly the rounded weights
-    // that P.V uses and costs one MFMA per chunk instead of 16 adds per lane.
-    // e4m3 carries p * scale into P.V, so it sums p on the VALU (l_run).
+    // that P.V uses and costs one MFMA per chunk instead of 16 adds per lane
+    // (e4m3 V carries its block scale in the widened values, so the weights
+    // are plain probabilities there too).
     f32x4_t lacc[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-    bf16x8_t ones;
+    PT ones;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) ones[e] = (__bf16)1.0f;
+    for (int e = 0; e < 8; ++e) ones[e] = (PE)1.0f;
 
     const int32_t *btr = a.block_tables + (int64_t)row * a.max_blocks_per_row;
     const int64_t blk_stride = (int64_t)a.num_kv_heads * 16 * D;
@@ -871,7 +892,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     auto tile_id = [&](int kt) -> int { return lids[min(4 * (kt - kt0) + bsel, nblk - 1)]; };
 
     Raw kreg[FP8 ? NJ : 1], vreg[FP8 ? NJ : 1];
-    float sreg = 0.f;
+    float sreg = 0.f, vscale = 1.f;
     auto issue_tile = [&](int kt, int buf, int id) {
         uint8_t *kl = lds + buf * LD::STAGE;
         uint8_t *vl = kl + LD::KBYTES;
@@ -892,13 +913,14 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                 kreg[j] = pool_load<false, Raw>(kb + k_off[j]);
                 vreg[j] = pool_load<false, Raw>(vb + v_off[j]);
             }
-            if (tid < 8) {
-                const int64_t si = (int64_t)blk_of(kt, tid & 3) * a.num_kv_heads + kvh;
-                sreg = tid < 4 ? a.k_scale[si] : a.v_scale[si];
-            }
+            // the V scale of this wave's block goes into the widened values;
+            // the K scales of the tile's four blocks scale the logits
+            vscale = a.v_scale[(int64_t)blk * a.num_kv_heads + kvh];
+            if (tid < 4) sreg = a.k_scale[(int64_t)blk_of(kt, tid) * a.num_kv_heads + kvh];
         }
     };
-    // e4m3 only: widen the staged registers into LDS
+    // e4m3 only: widen the staged registers into LDS, V times its block's
+    // scale as fp16
     auto store_tile = [&](int buf) {
         if constexpr (FP8) {
             uint8_t *kl = lds + buf * LD::STAGE;
@@ -907,10 +929,13 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
             for (int j = 0; j < NJ; ++j) {
                 *(u32x4_t *)(kl + (wave * NJ + j) * 1024 + 16 * lane) =
                     __builtin_bit_cast(u32x4_t, kv::widen(kreg[j]));
-                *(u32x4_t *)(vl + (wave * NJ + j) * 1024 + 16 * lane) =
-                    __builtin_bit_cast(u32x4_t, kv::widen(vreg[j]));
+                const bf16x8_t w = kv::widen(vreg[j]);
+                PT v;
+#pragma unroll
+                for (int e = 0; e < 8; ++e) v[e] = (PE)((float)w[e] * vscale);
+                *(u32x4_t *)(vl + (wave * NJ + j) * 1024 + 16 * lane) = __builtin_bit_cast(u32x4_t, v);
             }
-            if (tid < 8) lscale[buf * 8 + tid] = sreg;
+            if (tid < 4) lscale[buf * 4 + tid] = sreg;
         }
     };
     // zero V of keys at or past key_end in the tile of buffer `buf`
@@ -937,7 +962,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // Probabilities are taken against a reference m_run (log2 units) fixed
     // for the tile; it moves at the end of the tile when the tile's max
     // exceeds it by more than 8 (rescaling acc and l), or, before a chunk's
-    // exponentials, when a chunk's max exceeds it by more than 64 (rare guard
+    // exponentials, when a chunk's max exceeds it by more than kGuard (rare guard
     // that also covers the first tile, where m_run is still -inf).  Both
     // tests take any lane whose own scores cross the threshold, which is the
     // same as the column's maximum crossing it.
@@ -962,15 +987,9 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // scale (e4m3), mask, and this lane's max over its 8 scores of each query
     // column in log2 units (the column's max over its 4 lanes is formed only
     // on the rare rescale path)
-    auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2],
-                    float &svc) {
+    auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2]) {
         float sk = scale;
-        svc = 1.f;
-        if constexpr (FP8) {
-            const int bi = 2 * ch + (g4 >> 1);
-            sk = scale * lscale[buf * 8 + bi];
-            svc = lscale[buf * 8 + 4 + bi];
-        }
+        if constexpr (FP8) sk = scale * lscale[buf * 4 + 2 * ch + (g4 >> 1)];
         const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
@@ -992,21 +1011,17 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
             const float alpha = m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mnew[nn]);
-            if constexpr (FP8) l_run[nn] *= alpha;
-            else lacc[nn] *= alpha;
+            lacc[nn] *= alpha;
 #pragma unroll
             for (int i = 0; i < NT; ++i) acc[nn][i] *= alpha;
             m_run[nn] = mnew[nn];
             m_neg[nn] = mnew[nn] == -INFINITY ? 0.f : -mnew[nn];
-            m_hi64[nn] = mnew[nn] + 64.f;
+            m_hig[nn] = mnew[nn] + kGuard;
             m_hi8[nn] = mnew[nn] + 8.f;
         }
     };
-    // exponentials of one chunk against m_run, packed to bf16.  e4m3: the
-    // probability times the block's V scale is carried as a bf16 pair hi + lo
-    // (P.V takes two MFMAs): one bf16 would round every term of the block
-    // by the same relative amount, up to 2^-9 of the output.
-    auto expo = [&](const f32x4_t (&sc)[2][2], float svc, bf16x8_t (&pf)[2], bf16x8_t (&pl)[2]) {
+    // exponentials of one chunk against m_run, packed to bf16
+    auto expo = [&](const f32x4_t (&sc)[2][2], PT (&pf)[2]) {
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
 #pragma unroll
@@ -1014,54 +1029,40 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     const float pe = __builtin_amdgcn_exp2f(__builtin_fmaf(sc[t][nn][r], f, m_neg[nn]));
-                    if constexpr (FP8) {
-                        l_run[nn] += pe;
-                        const float x = pe * svc;
-                        const __bf16 hb = (__bf16)x;
-                        pf[nn][4 * t + r] = hb;
-                        pl[nn][4 * t + r] = (__bf16)(x - (float)hb);
-                    } else {
-                        pf[nn][4 * t + r] = (__bf16)pe;
-                    }
+                    pf[nn][4 * t + r] = (PE)pe;
                 }
         }
     };
-    auto pv = [&](const uint8_t *vl, int ch, const bf16x8_t (&pf)[2], const bf16x8_t (&pl)[2]) {
+    auto pv = [&](const uint8_t *vl, int ch, const PT (&pf)[2]) {
         const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + c16 * 32 +
                               16 * ((g4 & 1) ^ ((c16 >> 3) & 1));
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
-            const bf16x8_t vf = *(const bf16x8_t *)(vrow + i * 16 * 32);
+            const PT vf = *(const PT *)(vrow + i * 16 * 32);
 #pragma unroll
-            for (int nn = 0; nn < 2; ++nn) {
-                acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pf[nn], acc[nn][i], 0, 0, 0);
-                if constexpr (FP8)
-                    acc[nn][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(vf, pl[nn], acc[nn][i], 0, 0, 0);
-            }
+            for (int nn = 0; nn < 2; ++nn) acc[nn][i] = mfma_pv(vf, pf[nn], acc[nn][i]);
         }
-        if constexpr (!FP8) {
 #pragma unroll
-            for (int nn = 0; nn < 2; ++nn)
-                lacc[nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones, pf[nn], lacc[nn], 0, 0, 0);
-        }
+        for (int nn = 0; nn < 2; ++nn)
+            lacc[nn] = mfma_pv(ones, pf[nn], lacc[nn]);
     };
     auto tile = [&](int buf, int kt, bool masked) {
         const uint8_t *kl = lds + buf * LD::STAGE;
         const uint8_t *vl = kl + LD::KBYTES;
         f32x4_t s0[2][2], s1[2][2];
-        float m0[2], m1[2], sv0, sv1;
-        bf16x8_t p0[2], p1[2], l0[2], l1[2];
+        float m0[2], m1[2];
+        PT p0[2], p1[2];
         qk(kl, 0, s0);
-        prep(buf, kt, 0, masked, s0, m0, sv0);
-        if (__any(m0[0] > m_hi64[0] || m0[1] > m_hi64[1])) {
+        prep(buf, kt, 0, masked, s0, m0);
+        if (__any(m0[0] > m_hig[0] || m0[1] > m_hig[1])) {
             const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m0[0])),
                                  fmaxf(m_run[1], wave_max_xor16_32(m0[1]))};
             rescale(mn);
         }
         qk(kl, 1, s1);          // MFMA ...
-        expo(s0, sv0, p0, l0);  // ... with the exponentials of chunk 0
-        prep(buf, kt, 1, masked, s1, m1, sv1);
-        if (__any(m1[0] > m_hi64[0] || m1[1] > m_hi64[1])) {
+        expo(s0, p0);           // ... with the exponentials of chunk 0
+        prep(buf, kt, 1, masked, s1, m1);
+        if (__any(m1[0] > m_hig[0] || m1[1] > m_hig[1])) {
             // chunk 0's probabilities, not yet added, move with the reference
             const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m1[0])),
                                  fmaxf(m_run[1], wave_max_xor16_32(m1[1]))};
@@ -1070,22 +1071,13 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
                 const float alpha =
                     m_run[nn] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[nn] - mn[nn]);
 #pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                    if constexpr (FP8) {
-                        const float x = ((float)p0[nn][e] + (float)l0[nn][e]) * alpha;
-                        const __bf16 hb = (__bf16)x;
-                        p0[nn][e] = hb;
-                        l0[nn][e] = (__bf16)(x - (float)hb);
-                    } else {
-                        p0[nn][e] = (__bf16)((float)p0[nn][e] * alpha);
-                    }
-                }
+                for (int e = 0; e < 8; ++e) p0[nn][e] = (PE)((float)p0[nn][e] * alpha);
             }
             rescale(mn);
         }
-        pv(vl, 0, p0, l0);      // MFMA ...
-        expo(s1, sv1, p1, l1);  // ... with the exponentials of chunk 1
-        pv(vl, 1, p1, l1);
+        pv(vl, 0, p0);          // MFMA ...
+        expo(s1, p1);           // ... with the exponentials of chunk 1
+        pv(vl, 1, p1);
         const float mt[2] = {vmax(m0[0], m1[0]), vmax(m0[1], m1[1])};
         if (__any(mt[0] > m_hi8[0] || mt[1] > m_hi8[1])) {
             const float mc[2] = {wave_max_xor16_32(mt[0]), wave_max_xor16_32(mt[1])};
@@ -1142,13 +1134,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 
 #pragma unroll
     for (int nn = 0; nn < 2; ++nn) {
-        float l_tot;
-        if constexpr (FP8) {
-            l_tot = l_run[nn] + __shfl_xor(l_run[nn], 16);
-            l_tot += __shfl_xor(l_tot, 32);
-        } else {
-            l_tot = lacc[nn][0];
-        }
+        const float l_tot = lacc[nn][0];
         if (!qok[nn]) continue;
         const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
         float *dst;

@@ -93,6 +93,24 @@ def test_many_rows(torch_cuda, kv):
     _check_small(w, torch_cuda, f"many-rows-{kv}")
 
 
+def _bf16_doubled(bits):
+    """bf16 bit patterns of twice the values (exact)."""
+    x = (bits.astype(np.uint32) << 16).view(np.float32) * np.float32(2.0)
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_fp8_queries_seeing_few_keys(torch_cuda):
+    # The first queries of prefill chunks that start at position 0 see one or
+    # two keys, so their outputs are single V values.  An e4m3 value times its
+    # block scale is not bf16-exact; with V doubled (|v| up to about 10) a
+    # bf16 P.V operand would be off by up to 2^-9 |v|, beyond the tolerance.
+    rows = [W.RowSpec(W.PREFILL, 0, 40), W.RowSpec(W.PREFILL, 0, 3), W.RowSpec(W.DECODE, 0, 1),
+            W.RowSpec(W.PREFILL, 0, 17)]
+    w = W.build("fp8-few-keys", rows, {}, 16, 4, 128, kv_dtype=W.KV_FP8, seed=23)
+    w.v_new = _bf16_doubled(w.v_new)
+    _check_small(w, torch_cuda, "fp8-few-keys")
+
+
 def _rows_case(name, n_decode, prefill_q, kv, seed):
     g = np.random.Generator(np.random.PCG64(seed))
     rows = [W.RowSpec(W.DECODE, int(g.integers(0, 80)), 1, int(g.integers(-1, 2)))
