@@ -29,7 +29,9 @@
  *   V codes  [num_blocks][num_kv_heads][head_dim][16]   (block-transposed)
  *   bf16 pools store bf16; e4m3 pools store OCP e4m3fn bytes plus fp32 scales
  *   k_scale / v_scale [num_blocks][num_kv_heads]: the value of a code is
- *   e4m3(code) * scale of its (block, head).
+ *   e4m3(code) * scale of its (block, head).  Chunked-prefill attention over
+ *   an e4m3 pool carries V values in fp16, so they must lie within +-65504
+ *   (finite results are not guaranteed beyond).
  * Token-major tensors: q [T][Hq][head_dim] bf16, k_new / v_new
  *   [T][Hkv][head_dim] bf16, out [T][Hq][head_dim] fp32, where token t of row
  *   r is q_start[r] + i for its i-th new token, at position
