@@ -212,6 +212,34 @@ def test_block_copy_many_pairs(torch_cuda):
         same_pool(it.pool_host(), pool)
 
 
+# block ids a prefill workgroup can stage in LDS at head_dim 128:
+# (160 KiB - 3 stages x 32 KiB - 3 x 16 B of scales) / 4 B; pinned on the host
+# by test_abi_host.test_prefill_row_beyond_the_staging_limit
+PF_MAX_BLOCKS_D128 = 16372
+
+
+def test_prefill_at_the_staging_limit(torch_cuda):
+    # one prefill row whose key range fills the block-id staging exactly:
+    # 8,448 new tokens after 253,504 cached ones, 4 KV heads (132 workgroups,
+    # more than half the CUs, so the key range is not cut into pieces)
+    q = 8448
+    w = W.build("pf-limit", [W.RowSpec(W.PREFILL, PF_MAX_BLOCKS_D128 * 16 - q, q)], {}, 4, 4, 128,
+                seed=31)
+    say(f"[case] prefill at the staging limit: T={w.batch.num_tokens} "
+        f"L={int(w.batch.seq_lens[0])} NB={w.num_blocks}")
+    it = _run(w, torch_cuda)
+    c, ids = compact(w)
+    pool = oracle.prepare(c)
+    oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
+    same_pool(it.pool_host(ids), pool)
+    sel = sample_queries(w, 48, seed=31)
+    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, sel=sel)
+    got = it.out.cpu().numpy().reshape(-1, w.head_dim)[sel]
+    err, nerr = attn_error(got, ref)
+    say(f"       {len(sel)} sampled outputs: max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
+
+
 @pytest.mark.parametrize("cfg", [2, 3, 4, 5])
 def test_full_size_config(torch_cuda, cfg):
     w = W.config(cfg)
