@@ -29,6 +29,8 @@ namespace echo {
 typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
 typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef float f32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // P.V products: bf16 (bf16 cache) or fp16 (e4m3 cache) operands, fp32 accumulate
 __device__ __forceinline__ f32x4_t mfma_pv(bf16x8_t a, bf16x8_t b, f32x4_t c) {
@@ -37,8 +39,6 @@ __device__ __forceinline__ f32x4_t mfma_pv(bf16x8_t a, bf16x8_t b, f32x4_t c) {
 __device__ __forceinline__ f32x4_t mfma_pv(f16x8_t a, f16x8_t b, f32x4_t c) {
     return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
 }
-typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
-typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
 
 // ------------------------------------------------------------------- codecs
 
@@ -737,11 +737,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // operand read onto distinct chunks, so every 16-lane read of 16 bytes per
 // lane touches all 64 LDS banks once (and 8-lane reads 32 banks once).
 // bf16 pools are copied global -> LDS directly (global_load_lds_dwordx4, no
-// staging registers); e4m3 pools go through registers and are widened to bf16
-// on the way in (K), or to fp16 after multiplication by the (block, head)
-// scale (V; K scales multiply the logits instead).  Tiles of keys at or past the last
-// token's position get
-// their V entries zeroed (0 * NaN is NaN for unwritten slots).
+// staging registers); e4m3 pools go through registers and are widened on the
+// way in: K to bf16, V to fp16 after multiplication by its (block, head) scale
+// (K scales multiply the logits instead).  Tiles of keys at or past the last
+// token's position get their V entries zeroed (0 * NaN is NaN for unwritten
+// slots).
 
 constexpr int kPfKeys = 64;
 constexpr int kPfLdsLimit = 160 * 1024;   // LDS of one gfx950 CU
@@ -962,10 +962,10 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     // Probabilities are taken against a reference m_run (log2 units) fixed
     // for the tile; it moves at the end of the tile when the tile's max
     // exceeds it by more than 8 (rescaling acc and l), or, before a chunk's
-    // exponentials, when a chunk's max exceeds it by more than kGuard (rare guard
-    // that also covers the first tile, where m_run is still -inf).  Both
-    // tests take any lane whose own scores cross the threshold, which is the
-    // same as the column's maximum crossing it.
+    // exponentials, when a chunk's max exceeds it by more than kGuard (rare
+    // guard that also covers the first tile, where m_run is still -inf).
+    // Both tests take any lane whose own scores cross the threshold, which is
+    // the same as the column's maximum crossing it.
     auto qk = [&](const uint8_t *kl, int ch, f32x4_t (&sc)[2][2]) {
 #pragma unroll
         for (int t = 0; t < 2; ++t) {
@@ -1020,7 +1020,7 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
             m_hi8[nn] = mnew[nn] + 8.f;
         }
     };
-    // exponentials of one chunk against m_run, packed to bf16
+    // exponentials of one chunk against m_run, packed to bf16 (fp16 for e4m3)
     auto expo = [&](const f32x4_t (&sc)[2][2], PT (&pf)[2]) {
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
