@@ -622,9 +622,27 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     pf.heads_per_chunk = plan.heads_per_chunk;
     pf.part_o = a.part_o;
     pf.part_lse = a.part_lse;
-    hipError_t e = launch_attention(a, m, pf, pool->head_dim, pool->dtype == ECHO_KV_FP8_E4M3, s,
-                                    ev ? ev + 2 : nullptr);
-    if (e != hipSuccess) return hip_fail(e, "attention launch");
+    const int D = pool->head_dim;
+    const bool fp8 = pool->dtype == ECHO_KV_FP8_E4M3;
+    hipError_t e;
+    // prefill, decode and merge in that order on the caller's stream; with
+    // profiling on, an event pair around each kernel that launches (an empty
+    // pair still costs GPU time between the two records)
+    if (pf.n_logical > 0) {
+        if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_prefill(pf, D, fp8, s)) != hipSuccess) return hip_fail(e, "prefill launch");
+        if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    if (a.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[4], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_decode(a, D, fp8, s)) != hipSuccess) return hip_fail(e, "decode launch");
+        if (ev && (e = hipEventRecord(ev[5], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    if (m.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[6], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_merge(m, D, s)) != hipSuccess) return hip_fail(e, "merge launch");
+        if (ev && (e = hipEventRecord(ev[7], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
     g_prof.valid = ev != nullptr;
     g_prof.launched[0] = true;
     g_prof.launched[1] = pf.n_logical > 0;

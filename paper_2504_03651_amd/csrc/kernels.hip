@@ -536,8 +536,10 @@ __device__ __forceinline__ int dec_logical(int P, int run_log2) {
     return ((round * 8 + xr) << run_log2) + (q & ((1 << run_log2) - 1));
 }
 
+// One decode workgroup of four waves: P is its physical workgroup index in
+// the decode order (dec_logical), tid its thread index in [0, 256).
 template <int D, bool FP8>
-__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+__device__ __forceinline__ void decode_body(const AttnArgs &a, int P, int tid) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
     typedef typename kv::VRaw VRaw;
@@ -545,9 +547,9 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     constexpr int NT = D / 16;            // 16-row d tiles of O^T
     constexpr int NK = D / kv::KSTEP;     // 16-byte K loads per key row and lane
 
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int64_t idx = (int64_t)dec_logical(blockIdx.x, a.run_log2) * 4 + wave;
+    const int lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int64_t idx = (int64_t)dec_logical(P, a.run_log2) * 4 + wave;
     if (idx >= a.n_waves) return;
     const int di = (int)(idx / a.waves_per_desc);
     const int rem = (int)(idx - (int64_t)di * a.waves_per_desc);
@@ -724,6 +726,11 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
     for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i + 4 * g4) = acc[i] * inv;
 }
 
+template <int D, bool FP8>
+__global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
+    decode_body<D, FP8>(a, blockIdx.x, threadIdx.x);
+}
+
 // ------------------------------------------------------------------ prefill
 //
 // One workgroup = 8 waves x 32 query vectors (consecutive tokens of one
@@ -771,8 +778,10 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) 
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
+// One prefill workgroup: P is its physical workgroup index in the prefill
+// grid (8 * per_xcd workgroups), all kPfThreads threads take part.
 template <int D, bool FP8>
-__global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(PrefillArgs a) {
+__device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
     typedef typename kv::VRaw Raw;   // 8 codes (16 or 8 bytes)
@@ -797,7 +806,6 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     float *lscale = (float *)(lds + kPfStages * LD::STAGE);  // [stage][4]: K scales
     int32_t *lids = (int32_t *)(lscale + kPfStages * 4);      // the row's block ids
 
-    const int P = blockIdx.x;
     const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
     if (L >= a.n_logical) return;
     const int kvh = L / a.n_pdesc;
@@ -1156,6 +1164,11 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
     }
 }
 
+template <int D, bool FP8>
+__global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(PrefillArgs a) {
+    prefill_body<D, FP8>(a, blockIdx.x);
+}
+
 // -------------------------------------------------------------------- merge
 
 template <int D>
@@ -1311,67 +1324,68 @@ int prefill_max_blocks(int head_dim) {
     return (kPfLdsLimit - (head_dim == 64 ? PfLds<64>::BYTES : PfLds<128>::BYTES)) / 4;
 }
 
-template <int D, bool FP8>
-static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
-    // the dynamic-LDS limit, raised once per device (bit d: done on device d;
-    // concurrent first calls both set it, which is harmless)
-    static std::atomic<uint64_t> attr_devices{0};
-    const int bytes = PfLds<D>::BYTES + 4 * p.max_blocks;
+// The dynamic-LDS limit of kernel f, raised once per device (bit d: done on
+// device d; concurrent first calls both set it, which is harmless).
+static hipError_t raise_lds_limit(const void *f, std::atomic<uint64_t> &done) {
     int dev = 0;
     hipError_t e = hipGetDevice(&dev);
     if (e != hipSuccess) return e;
     const uint64_t bit = dev >= 0 && dev < 64 ? (1ull << dev) : 0;
-    if (!bit || !(attr_devices.load(std::memory_order_acquire) & bit)) {
-        e = hipFuncSetAttribute((const void *)prefill_kernel<D, FP8>,
-                                hipFuncAttributeMaxDynamicSharedMemorySize, kPfLdsLimit);
+    if (!bit || !(done.load(std::memory_order_acquire) & bit)) {
+        e = hipFuncSetAttribute(f, hipFuncAttributeMaxDynamicSharedMemorySize, kPfLdsLimit);
         if (e != hipSuccess) return e;
-        attr_devices.fetch_or(bit, std::memory_order_release);
+        done.fetch_or(bit, std::memory_order_release);
     }
+    return hipSuccess;
+}
+
+template <int D, bool FP8>
+static hipError_t launch_prefill_t(const PrefillArgs &p, hipStream_t s) {
+    static std::atomic<uint64_t> attr_devices{0};
+    hipError_t e = raise_lds_limit((const void *)prefill_kernel<D, FP8>, attr_devices);
+    if (e != hipSuccess) return e;
+    const int bytes = PfLds<D>::BYTES + 4 * p.max_blocks;
     const dim3 grid((unsigned)(8 * p.per_xcd)), block(kPfThreads);
     hipLaunchKernelGGL((prefill_kernel<D, FP8>), grid, block, bytes, s, p);
     return hipGetLastError();
 }
 
-hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
-                            int head_dim, bool fp8, hipStream_t s, hipEvent_t *ev) {
-    hipError_t e;
-    // event pairs only around kernels that launch: an empty pair still costs
-    // GPU time between the two records
-    if (p.n_logical > 0) {
-        if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return e;
-        if (head_dim == 64 && !fp8) e = launch_prefill_t<64, false>(p, s);
-        else if (head_dim == 64) e = launch_prefill_t<64, true>(p, s);
-        else if (!fp8) e = launch_prefill_t<128, false>(p, s);
-        else e = launch_prefill_t<128, true>(p, s);
-        if (e != hipSuccess) return e;
-        if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return e;
-    }
-    if (a.n_waves > 0) {
-        if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return e;
-        // runs of 16 workgroups, or shorter so that there are at least 64 runs;
-        // a multiple of 8 runs, logical workgroups past the end exit at once
-        const int64_t nwg = (a.n_waves + 3) / 4;
-        AttnArgs b = a;
-        b.run_log2 = 4;
-        while (b.run_log2 > 0 && ((int64_t)64 << b.run_log2) > nwg) --b.run_log2;
-        const int64_t round = (int64_t)8 << b.run_log2;
-        const dim3 grid((unsigned)((nwg + round - 1) / round * round)), block(256);
-        if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, b);
-        else if (head_dim == 64) hipLaunchKernelGGL((attn_kernel<64, true>), grid, block, 0, s, b);
-        else if (!fp8) hipLaunchKernelGGL((attn_kernel<128, false>), grid, block, 0, s, b);
-        else hipLaunchKernelGGL((attn_kernel<128, true>), grid, block, 0, s, b);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return e;
-    }
-    if (m.n_waves > 0) {
-        if (ev && (e = hipEventRecord(ev[4], s)) != hipSuccess) return e;
-        const dim3 grid((unsigned)((m.n_waves + 3) / 4)), block(256);
-        if (head_dim == 64) hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, s, m);
-        else hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, s, m);
-        if ((e = hipGetLastError()) != hipSuccess) return e;
-        if (ev && (e = hipEventRecord(ev[5], s)) != hipSuccess) return e;
-    }
-    return hipSuccess;
+hipError_t launch_prefill(const PrefillArgs &p, int head_dim, bool fp8, hipStream_t s) {
+    if (p.n_logical <= 0) return hipSuccess;
+    if (head_dim == 64 && !fp8) return launch_prefill_t<64, false>(p, s);
+    if (head_dim == 64) return launch_prefill_t<64, true>(p, s);
+    if (!fp8) return launch_prefill_t<128, false>(p, s);
+    return launch_prefill_t<128, true>(p, s);
+}
+
+// Decode launch shape: runs of 16 workgroups, or shorter so that there are
+// at least 64 runs; the grid is a multiple of 8 runs (logical workgroups
+// past the end exit at once).  Returns the grid size and sets b.run_log2.
+static int64_t decode_grid(AttnArgs &b) {
+    const int64_t nwg = (b.n_waves + 3) / 4;
+    b.run_log2 = 4;
+    while (b.run_log2 > 0 && ((int64_t)64 << b.run_log2) > nwg) --b.run_log2;
+    const int64_t round = (int64_t)8 << b.run_log2;
+    return (nwg + round - 1) / round * round;
+}
+
+hipError_t launch_decode(const AttnArgs &a, int head_dim, bool fp8, hipStream_t s) {
+    if (a.n_waves <= 0) return hipSuccess;
+    AttnArgs b = a;
+    const dim3 grid((unsigned)decode_grid(b)), block(256);
+    if (head_dim == 64 && !fp8) hipLaunchKernelGGL((attn_kernel<64, false>), grid, block, 0, s, b);
+    else if (head_dim == 64) hipLaunchKernelGGL((attn_kernel<64, true>), grid, block, 0, s, b);
+    else if (!fp8) hipLaunchKernelGGL((attn_kernel<128, false>), grid, block, 0, s, b);
+    else hipLaunchKernelGGL((attn_kernel<128, true>), grid, block, 0, s, b);
+    return hipGetLastError();
+}
+
+hipError_t launch_merge(const MergeArgs &m, int head_dim, hipStream_t s) {
+    if (m.n_waves <= 0) return hipSuccess;
+    const dim3 grid((unsigned)((m.n_waves + 3) / 4)), block(256);
+    if (head_dim == 64) hipLaunchKernelGGL((merge_kernel<64>), grid, block, 0, s, m);
+    else hipLaunchKernelGGL((merge_kernel<128>), grid, block, 0, s, m);
+    return hipGetLastError();
 }
 
 }  // namespace echo

@@ -79,10 +79,11 @@ hipError_t launch_plan_upload(const void *src, void *dst, int64_t words, hipStre
 // Largest number of block ids the prefill kernel can stage for one row.
 int prefill_max_blocks(int head_dim);
 
-// Launches prefill, decode and merge kernels in that order.  With `ev` set,
-// records ev[2k] before and ev[2k+1] after kernel k (0 prefill, 1 decode,
-// 2 merge), for the kernels that launch.
-hipError_t launch_attention(const AttnArgs &a, const MergeArgs &m, const PrefillArgs &p,
-                            int head_dim, bool fp8, hipStream_t s, hipEvent_t *ev);
+// Attention launchers; each returns hipSuccess without launching when it
+// has no work.  The merge reads the partial results of both others, so it
+// runs after them.
+hipError_t launch_prefill(const PrefillArgs &p, int head_dim, bool fp8, hipStream_t s);
+hipError_t launch_decode(const AttnArgs &a, int head_dim, bool fp8, hipStream_t s);
+hipError_t launch_merge(const MergeArgs &m, int head_dim, hipStream_t s);
 
 }  // namespace echo
