@@ -217,6 +217,17 @@ int plan_for(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_
                       plan_options(pool), plan);
 }
 
+// Shortest XCD run (log2 of decode workgroups) for a plan: the waves that
+// read one shared key range are consecutive in the work order, and a run
+// twice their span keeps most such groups inside one XCD's L2 (a group that
+// straddles two runs is fetched from HBM by both XCDs).
+int run_log2_for(int32_t sibling_waves) {
+    const int64_t wgs = 2 * (((int64_t)sibling_waves + 3) / 4);
+    int l = 0;
+    while (l < 5 && ((int64_t)1 << l) < wgs) ++l;
+    return l;
+}
+
 // Pinned host staging for plan uploads: a small ring per device, each slot
 // guarded by an event so that a buffer is refilled only after the kernel
 // that copies it to the workspace has completed.
@@ -569,6 +580,7 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     a.desc = (const WorkDesc *)(w + L.off_desc);
     a.n_waves = L.n_desc * plan.waves_per_desc;
     a.waves_per_desc = plan.waves_per_desc;
+    a.run_log2 = run_log2_for(plan.sibling_waves);
     a.head_chunks = plan.head_chunks;
     a.heads_per_chunk = plan.heads_per_chunk;
     a.group = num_q_heads / pool->num_kv_heads;

@@ -1359,12 +1359,16 @@ hipError_t launch_prefill(const PrefillArgs &p, int head_dim, bool fp8, hipStrea
 }
 
 // Decode launch shape: runs of 16 workgroups, or shorter so that there are
-// at least 64 runs; the grid is a multiple of 8 runs (logical workgroups
-// past the end exit at once).  Returns the grid size and sets b.run_log2.
+// at least 64 runs, but never shorter than the run length the caller asks
+// for in b.run_log2 (at most 32 workgroups); the grid is a multiple of 8 runs
+// (logical workgroups past the end exit at once).  Returns the grid size and
+// sets b.run_log2.
 static int64_t decode_grid(AttnArgs &b) {
     const int64_t nwg = (b.n_waves + 3) / 4;
+    const int min_log2 = std::min(std::max(b.run_log2, 0), 5);
     b.run_log2 = 4;
     while (b.run_log2 > 0 && ((int64_t)64 << b.run_log2) > nwg) --b.run_log2;
+    b.run_log2 = std::max(b.run_log2, min_log2);
     const int64_t round = (int64_t)8 << b.run_log2;
     return (nwg + round - 1) / round * round;
 }

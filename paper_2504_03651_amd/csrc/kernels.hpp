@@ -40,7 +40,7 @@ struct AttnArgs {
     int32_t max_blocks_per_row;
     float scale_log2;               // sm_scale * log2(e)
     float *out, *part_o, *part_lse;
-    int32_t run_log2;               // XCD run length (set by the launcher)
+    int32_t run_log2;               // XCD run length: the caller's minimum, set by the launcher
 };
 
 struct PrefillArgs {

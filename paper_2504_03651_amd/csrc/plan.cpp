@@ -165,6 +165,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
 
     int64_t n_slots = 0;
     const int64_t wpd = plan.waves_per_desc;
+    plan.sibling_waves = 0;
     for (size_t si = 0; si < segs.size(); ++si) {
         const Segment &s = segs[si];
         const int32_t tok_base = (int32_t)plan.tok_list.size();
@@ -173,6 +174,9 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
         const int32_t rep = seg_rows[s.rows_off];
         const bool direct = (s.nrows == 1 && cnt[rep] == 1);
         const bool shared = s.nrows > nt_max || nhc > 1;
+        if (s.nrows > 1)   // slices x KV heads x head chunks read each piece
+            plan.sibling_waves = (int32_t)std::max<int64_t>(
+                plan.sibling_waves, (s.nrows + nt_max - 1) / nt_max * wpd);
         plan.stats.decode_kv_tokens += s.key_end - kBlock * s.j0;
         for (int32_t j = s.j0; j < s.j1; j += split) {
             const int32_t jend = std::min(j + split, s.j1);

@@ -127,6 +127,7 @@ struct Plan {
     PlanLayout layout;
     PlanStats stats;
     int32_t waves_per_desc = 1;   // num_kv_heads * head_chunks
+    int32_t sibling_waves = 0;    // most decode waves that read one shared key range
     int32_t head_chunks = 1;
     int32_t heads_per_chunk = 1;  // min(G, 16)
 };
