@@ -173,7 +173,10 @@ int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
  *                           for nt == 1 the token and its key limit (else -1, 0)
  *   pdesc     [n_pdesc][8]  prefill work: row, tok0, ntok, key_end,
  *                           key_begin, part, kfull (keys every token of the
- *                           tile sees), 0
+ *                           tile sees), next (1 + index of a descriptor the
+ *                           same workgroup runs afterwards, or 0; descriptors
+ *                           named this way come last and get no workgroup
+ *                           of their own)
  *   tok_list  [n_tok_list]  tokens of the decode slices
  *   klim      [n_tokens]    keys visible to each token
  *   merge_tok [n_merge_rows], merge_ptr [n_merge_rows + 1]

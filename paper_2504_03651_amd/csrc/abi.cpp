@@ -613,8 +613,8 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     m.out = out;
     PrefillArgs pf;
     pf.pdesc = (const PrefillDesc *)(w + L.off_pdesc);
-    pf.n_pdesc = (int32_t)L.n_pdesc;
-    pf.n_logical = (int32_t)(L.n_pdesc * pool->num_kv_heads);
+    pf.n_pdesc = plan.pdesc_grid;   // chained descriptors follow these
+    pf.n_logical = (int32_t)((int64_t)plan.pdesc_grid * pool->num_kv_heads);
     pf.per_xcd = (pf.n_logical + 7) / 8;
     pf.group = a.group;
     pf.klim = a.klim;

@@ -778,10 +778,10 @@ constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) 
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
-// One prefill workgroup: P is its physical workgroup index in the prefill
-// grid (8 * per_xcd workgroups), all kPfThreads threads take part.
+// One prefill descriptor di (a tile's tokens, or a piece of their keys) for
+// KV head kvh; all kPfThreads threads of the workgroup take part.
 template <int D, bool FP8>
-__device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
+__device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int di) {
     typedef KV<FP8> kv;
     typedef typename kv::T KT;
     typedef typename kv::VRaw Raw;   // 8 codes (16 or 8 bytes)
@@ -806,10 +806,6 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
     float *lscale = (float *)(lds + kPfStages * LD::STAGE);  // [stage][4]: K scales
     int32_t *lids = (int32_t *)(lscale + kPfStages * 4);      // the row's block ids
 
-    const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
-    if (L >= a.n_logical) return;
-    const int kvh = L / a.n_pdesc;
-    const int di = L - kvh * a.n_pdesc;
     const int32_t *dp = (const int32_t *)(a.pdesc + di);
     const int row = __builtin_amdgcn_readfirstlane(dp[0]);
     const int tok0 = __builtin_amdgcn_readfirstlane(dp[1]);
@@ -1161,6 +1157,24 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
         }
 #pragma unroll
         for (int i = 0; i < NT; ++i) *(f32x4_t *)(dst + 16 * i) = acc[nn][i] * inv;
+    }
+}
+
+// One prefill workgroup: P is its physical workgroup index in the prefill
+// grid (8 * per_xcd workgroups).  Its descriptor may name a second one
+// (a piece of another tile's keys) that the workgroup runs next.
+template <int D, bool FP8>
+__device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
+    const int L = (P % 8) * a.per_xcd + P / 8;  // consecutive logical tiles share an XCD
+    if (L >= a.n_logical) return;
+    const int kvh = L / a.n_pdesc;
+    int di = L - kvh * a.n_pdesc;
+    for (;;) {
+        prefill_piece<D, FP8>(a, kvh, di);
+        const int next = __builtin_amdgcn_readfirstlane(((const int32_t *)(a.pdesc + di))[7]);
+        if (next <= 0) break;
+        __syncthreads();   // the next descriptor refills the LDS ring and block ids
+        di = next - 1;
     }
 }
 

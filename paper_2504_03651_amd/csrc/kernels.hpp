@@ -45,7 +45,7 @@ struct AttnArgs {
 
 struct PrefillArgs {
     const PrefillDesc *pdesc;
-    int32_t n_pdesc;
+    int32_t n_pdesc;                // descriptors that get workgroups (chained ones follow)
     int32_t n_logical;              // n_pdesc * num_kv_heads
     int32_t per_xcd;                // logical tiles per XCD slot
     int32_t group;                  // Hq / Hkv (<= 128)

@@ -228,7 +228,7 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             d.key_begin = 0;
             d.part = -1;
             d.kfull = d.key_end - d.ntok + 1;
-            d.pad0 = 0;
+            d.next = 0;
             plan.pdesc.push_back(d);
             pf_work += (d.key_end + kPrefillTileKeys - 1) / kPrefillTileKeys;
             ++pf_tiles;
@@ -239,7 +239,9 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     // cut key ranges longer than the average share of a CU into pieces at
     // tile boundaries that every token of the tile sees unmasked.  Pieces
     // write partial softmax states that the merge kernel combines.  (With
-    // about one workgroup per CU the merge costs what the balance gains.)
+    // about one workgroup per CU, cutting every long range costs in the
+    // merge what it gains; the branch below moves only the excess.)
+    int32_t grid_pdesc = -1;   // descriptors that get workgroups (chained ones follow)
     if (pf_tiles > 0 && 2 * pf_tiles * Hkv <= (int64_t)opt.num_cus) {
         const int64_t share = (pf_work * Hkv + opt.num_cus - 1) / opt.num_cus;
         const int32_t piece = (int32_t)std::max<int64_t>(kPrefillMinPieceTiles, share);
@@ -285,7 +287,86 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             return x.key_end - x.key_begin > y.key_end - y.key_begin;
         });
         plan.pdesc.swap(out);
+    } else if (pf_tiles > 1 && pf_tiles * Hkv <= (int64_t)opt.num_cus) {
+        // One round of workgroups takes as long as its longest tile, and the
+        // causal tiles of a chunk span from its context to its full length.
+        // Short tiles' workgroups take over the leading keys of long tiles
+        // (keys every token of such a tile sees) as further descriptors
+        // chained to their own, so that every workgroup walks about the mean
+        // number of 64-key tiles.  All pieces of a long tile write partial
+        // states that the merge kernel combines.
+        const int32_t n = (int32_t)plan.pdesc.size();
+        std::vector<int32_t> &wk = plan.bounds;   // 64-key tiles per workgroup
+        std::vector<int32_t> &order = plan.bucket;
+        wk.resize(n);
+        order.resize(n);
+        int64_t total = 0;
+        for (int32_t i = 0; i < n; ++i) {
+            wk[i] = (plan.pdesc[i].key_end + kPrefillTileKeys - 1) / kPrefillTileKeys;
+            total += wk[i];
+            order[i] = i;
+        }
+        const int32_t target = (int32_t)((total + n - 1) / n);
+        std::stable_sort(order.begin(), order.end(),
+                         [&](int32_t x, int32_t y) { return wk[x] > wk[y]; });
+        std::vector<PrefillDesc> &chained = plan.pdesc_split;
+        chained.clear();
+        if (!plan.merge_ptr.empty()) plan.merge_ptr.pop_back();   // reopen the list
+        int32_t lo = n - 1;   // shortest tile that may still take a piece
+        std::vector<int32_t> &cuts = plan.cuts, &takers = plan.takers, &last = plan.ctail;
+        last.resize(n);   // last descriptor of each workgroup's chain
+        for (int32_t i = 0; i < n; ++i) last[i] = i;
+        for (int32_t hi = 0; hi < lo; ++hi) {
+            PrefillDesc &dj = plan.pdesc[order[hi]];
+            int32_t excess = wk[order[hi]] - target;
+            if (excess < kPrefillMinChainTiles) break;   // the rest have less
+            // leading pieces [cuts[k], cuts[k+1]) go to short tiles' workgroups
+            const int32_t unmasked = dj.kfull / kPrefillTileKeys;
+            cuts.assign(1, 0);
+            takers.clear();
+            while (excess >= kPrefillMinChainTiles) {
+                while (lo > hi && target - wk[order[lo]] < kPrefillMinChainTiles) --lo;
+                if (lo <= hi) break;
+                const int32_t i = order[lo];
+                const int32_t x = std::min(std::min(excess, target - wk[i]), unmasked - cuts.back());
+                if (x < kPrefillMinChainTiles) break;
+                cuts.push_back(cuts.back() + x);
+                takers.push_back(i);
+                wk[i] += x;
+                excess -= x;
+            }
+            if (takers.empty()) continue;
+            const int32_t np = (int32_t)takers.size() + 1;   // pieces of this tile
+            const int32_t slots = Hkv * nhc * dj.ntok * hpc;
+            for (int32_t t = 0; t < dj.ntok; ++t) {
+                plan.merge_tok.push_back(dj.tok0 + t);
+                plan.merge_ptr.push_back((int32_t)(plan.merge_ent.size() / 2));
+                for (int32_t p = 0; p < np; ++p) {
+                    plan.merge_ent.push_back((int32_t)(n_slots + (int64_t)p * slots));
+                    plan.merge_ent.push_back(dj.ntok | (t << 10));
+                }
+            }
+            for (int32_t p = 0; p + 1 < np; ++p) {
+                PrefillDesc head = dj;
+                head.key_begin = cuts[p] * kPrefillTileKeys;
+                head.key_end = cuts[p + 1] * kPrefillTileKeys;
+                head.part = (int32_t)(n_slots + (int64_t)p * slots);
+                const int32_t idx = n + (int32_t)chained.size();
+                int32_t &tail = last[takers[p]];
+                (tail < n ? plan.pdesc[tail] : chained[tail - n]).next = idx + 1;
+                tail = idx;
+                chained.push_back(head);
+            }
+            dj.key_begin = cuts.back() * kPrefillTileKeys;
+            dj.part = (int32_t)(n_slots + (int64_t)(np - 1) * slots);
+            wk[order[hi]] -= cuts.back();
+            n_slots += (int64_t)np * slots;
+        }
+        plan.merge_ptr.push_back((int32_t)(plan.merge_ent.size() / 2));
+        plan.pdesc.insert(plan.pdesc.end(), chained.begin(), chained.end());
+        grid_pdesc = n;
     }
+    plan.pdesc_grid = grid_pdesc >= 0 ? grid_pdesc : (int32_t)plan.pdesc.size();
     plan.stats.prefill_items = (int64_t)plan.pdesc.size() * Hkv;
     n_ent = (int64_t)plan.merge_ent.size() / 2;
 

@@ -56,11 +56,13 @@ struct PrefillDesc {   // 32 bytes
     int32_t key_begin; // first key of the piece, a multiple of the 64-key tile
     int32_t part;      // first partial slot of the piece, or -1: write `out`
     int32_t kfull;     // keys every token of the tile sees (unmasked below)
-    int32_t pad0;
+    int32_t next;      // 1 + index of a descriptor the same workgroup runs
+                       // after this one, or 0
 };
 static_assert(sizeof(PrefillDesc) == 32, "prefill descriptor layout");
 constexpr int kPrefillTileKeys = 64;      // keys per LDS tile of the prefill kernel
 constexpr int kPrefillMinPieceTiles = 8;  // shortest piece a long key range is cut into
+constexpr int kPrefillMinChainTiles = 2;  // fewest 64-key tiles moved to a chained piece
 // Decode key ranges are cut into pieces of about kSplitBytes of K+V per KV
 // head: 48 blocks of bf16 at head_dim 128, 96 of e4m3, whose waves move half
 // the bytes per block (a sweep of 16-128 blocks on the decode-only, mixed and
@@ -119,11 +121,12 @@ struct PlanOptions {
 struct Plan {
     std::vector<WorkDesc> desc, desc_sorted;
     std::vector<PrefillDesc> pdesc, pdesc_split;
+    int32_t pdesc_grid = 0;       // leading descriptors of pdesc that get workgroups
     std::vector<int32_t> bounds;
     int32_t prefill_tokens_per_tile = 1;
     std::vector<int32_t> tok_list, klim, merge_tok, merge_ptr, merge_ent;
     // scratch
-    std::vector<int32_t> nro, rows, tail_start, seg_rows, cnt, moff, cursor, bucket;
+    std::vector<int32_t> nro, rows, tail_start, seg_rows, cnt, moff, cursor, bucket, cuts, takers, ctail;
     PlanLayout layout;
     PlanStats stats;
     int32_t waves_per_desc = 1;   // num_kv_heads * head_chunks

@@ -133,15 +133,16 @@ def test_attention_rejects_non_positive_scale(scale):
 
 def test_prefill_row_beyond_the_staging_limit():
     # a prefill workgroup stages its row's block ids in LDS: one block more
-    # than fits (16,372 at head_dim 128) is refused before any work
+    # than fits (16,372 at head_dim 128) is refused before any work (GQA 8/4:
+    # 264 workgroups, so the tile's key range is not cut into pieces)
     q = 8448
-    w = W.build("pf-limit+1", [W.RowSpec(W.PREFILL, 16373 * 16 - q, q)], {}, 4, 4, 128, seed=31)
+    w = W.build("pf-limit+1", [W.RowSpec(W.PREFILL, 16373 * 16 - q, q)], {}, 8, 4, 128, seed=31)
     cp, cb, keep = _structs(w)
     L = echo.lib()
-    n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 8)
     assert n > 0
     fake = ctypes.c_void_p(256)   # never dereferenced: the check comes first
-    rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 4, 0.088, fake, fake, n, None)
+    rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 8, 0.088, fake, fake, n, None)
     assert rc == echo.ECHO_E_UNSUPPORTED
     assert "16373 blocks exceeds the 16372-block limit" in echo.last_error()
 

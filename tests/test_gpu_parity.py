@@ -144,6 +144,17 @@ def test_prefill_split_key_ranges(torch_cuda, hq, hkv, d, kv):
     _check_small(w, torch_cuda, f"prefill-split-{hq}/{hkv}/{d}/{kv}")
 
 
+@pytest.mark.parametrize("kv", [W.KV_BF16, W.KV_FP8])
+def test_prefill_one_round_chained(torch_cuda, kv):
+    # one round of prefill workgroups (24 tiles x 8 KV heads, tiles of 1 to 40
+    # 64-key tiles; the same shape as the plan-invariant case): short tiles'
+    # workgroups also run the leading keys of long tiles, chained
+    rows = [W.RowSpec(W.PREFILL, 0, 1024), W.RowSpec(W.DECODE, 900, 1),
+            W.RowSpec(W.PREFILL, 2000, 512), W.RowSpec(W.DECODE, 40, 1)]
+    w = W.build(f"one-round-{kv}", rows, {}, 32, 8, 128, kv_dtype=kv, seed=131)
+    _check_small(w, torch_cuda, f"prefill-one-round-{kv}")
+
+
 def test_deterministic(torch_cuda):
     w = W.random_case(110, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
                       max_ctx=2000, max_q=64)
@@ -220,10 +231,11 @@ PF_MAX_BLOCKS_D128 = 16372
 
 def test_prefill_at_the_staging_limit(torch_cuda):
     # one prefill row whose key range fills the block-id staging exactly:
-    # 8,448 new tokens after 253,504 cached ones, 4 KV heads (132 workgroups,
-    # more than half the CUs, so the key range is not cut into pieces)
+    # 8,448 new tokens after 253,504 cached ones, GQA 8/4 (66 tiles x 4 KV
+    # heads = 264 workgroups, more than one round, so the key range is
+    # neither cut into pieces nor shared out to chained workgroups)
     q = 8448
-    w = W.build("pf-limit", [W.RowSpec(W.PREFILL, PF_MAX_BLOCKS_D128 * 16 - q, q)], {}, 4, 4, 128,
+    w = W.build("pf-limit", [W.RowSpec(W.PREFILL, PF_MAX_BLOCKS_D128 * 16 - q, q)], {}, 8, 4, 128,
                 seed=31)
     say(f"[case] prefill at the staging limit: T={w.batch.num_tokens} "
         f"L={int(w.batch.seq_lens[0])} NB={w.num_blocks}")

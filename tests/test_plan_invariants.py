@@ -8,7 +8,10 @@ the CPU instead of as a wrong address on the GPU:
   * for every new token, the key ranges of the work items that cover it tile
     [0, keys visible to it) exactly once, and a token with several items has
     one merge row whose entries are exactly those items;
-  * partial-slot ranges of different items never overlap.
+  * partial-slot ranges of different items never overlap;
+  * a prefill descriptor chained to another one (run next by the same
+    workgroup) is named once and comes after every descriptor with a
+    workgroup of its own; chains end.
 """
 import numpy as np
 import pytest
@@ -17,6 +20,14 @@ from paper_2504_03651_amd import echo
 from paper_2504_03651_amd import workload as W
 
 TILE = 64   # keys per prefill LDS tile
+
+
+def _one_round_case(kv=W.KV_BF16):
+    # 24 prefill tiles x 8 KV heads: one round of workgroups on 256 CUs, with
+    # tiles of 1 to 40 64-key tiles
+    rows = [W.RowSpec(W.PREFILL, 0, 1024), W.RowSpec(W.DECODE, 900, 1),
+            W.RowSpec(W.PREFILL, 2000, 512), W.RowSpec(W.DECODE, 40, 1)]
+    return W.build(f"one-round-{kv}", rows, {}, 32, 8, 128, kv_dtype=kv, seed=131)
 
 
 def _cases():
@@ -32,6 +43,7 @@ def _cases():
                 W.RowSpec(W.PREFILL, 1500, 300), W.RowSpec(W.PREFILL, 64, 17)]
         yield W.build(f"split-{hq}-{hkv}", rows, {}, hq, hkv, 128, seed=118)
     yield W.config(3)
+    yield _one_round_case()
     yield W.random_case(205, num_rows=600, num_q_heads=4, num_kv_heads=2, head_dim=64,
                         max_ctx=100, max_q=30, n_groups=3)
 
@@ -84,6 +96,21 @@ def test_plan_invariants(w):
     mtok = region(lay["off_merge_tok"], lay["n_merge_rows"])
     mptr = region(lay["off_merge_ptr"], lay["n_merge_rows"] + 1)
     ment = region(lay["off_merge_ent"], lay["n_merge_entries"], 2)
+
+    # ---- chained prefill descriptors
+    nxt = pdesc[:, 7].astype(np.int64) if len(pdesc) else np.zeros(0, np.int64)
+    targets = (nxt[nxt > 0] - 1).tolist()
+    assert len(set(targets)) == len(targets), "a descriptor is chained twice"
+    n_grid = len(pdesc) - len(targets)
+    assert all(n_grid <= t < len(pdesc) for t in targets)
+    seen = 0
+    for i in range(n_grid):   # each chain ends (targets are named once: no cycle)
+        j = i
+        while nxt[j] > 0:
+            j = int(nxt[j]) - 1
+            seen += 1
+            assert pdesc[j][5] >= 0, "a chained piece writes partial states"
+    assert seen == len(targets), "a chained descriptor is not reachable"
 
     # ---- per-token keys and rows
     q = np.diff(b.q_start)
@@ -171,6 +198,40 @@ def test_split_pieces_present():
     lay, words = _decode(w)
     pd = words[lay["off_pdesc"]:lay["off_pdesc"] + 8 * lay["n_pdesc"]].reshape(-1, 8)
     assert (pd[:, 5] >= 0).any() and (pd[:, 4] > 0).any()
+
+
+def _prefill_work(w):
+    """64-key tiles walked per prefill workgroup (own descriptor plus the
+    chained one), and per tile before any balancing."""
+    lay, words = _decode(w)
+    pd = words[lay["off_pdesc"]:lay["off_pdesc"] + 8 * lay["n_pdesc"]].reshape(-1, 8)
+    tiles = lambda d: (int(d[3]) - int(d[4]) + TILE - 1) // TILE
+    n_grid = len(pd) - int((pd[:, 7] > 0).sum())
+    work = []
+    for i in range(n_grid):
+        j, t = i, tiles(pd[i])
+        while pd[j, 7] > 0:
+            j = int(pd[j, 7]) - 1
+            t += tiles(pd[j])
+        work.append(t)
+    orig = [(int(pd[i, 3]) + TILE - 1) // TILE for i in range(n_grid)]
+    return work, orig, int((pd[:, 7] > 0).sum())
+
+
+def test_one_round_prefill_balanced():
+    # the mixed batch's 2,048-token chunk on 1,024 cached tokens: 32 tiles of
+    # 17..48 64-key tiles per KV head, 256 workgroups; the longest workgroup
+    # walks 34 (mean 32.5; a tile only 1 over the target of 33 keeps its keys)
+    work, orig, chains = _prefill_work(W.config(3))
+    assert max(orig) == 48 and chains == 14
+    assert max(work) == 34 and sum(work) == sum(orig)
+    # two chunks of unequal lengths (tiles of 1..16 and 33..40, mean 17.8): a
+    # long tile gives pieces to several short ones and a short one takes
+    # pieces of several long ones
+    work, orig, chains = _prefill_work(_one_round_case())
+    assert max(orig) == 40 and max(work) == 19 and sum(work) == sum(orig)
+    # more than one round of workgroups: no chains
+    assert _prefill_work(W.config(5))[2] == 0
 
 
 def test_plan_pack_buffer_too_small():
