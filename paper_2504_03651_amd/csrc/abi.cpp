@@ -600,7 +600,7 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     a.part_o = (float *)(w + L.off_part_o);
     a.part_lse = (float *)(w + L.off_part_lse);
     MergeArgs m;
-    m.n_waves = L.n_merge_rows * num_q_heads;
+    m.n_waves = L.n_merge_rows * ((num_q_heads + 3) / 4);
     m.num_q_heads = num_q_heads;
     m.head_chunks = plan.head_chunks;
     m.heads_per_chunk = plan.heads_per_chunk;

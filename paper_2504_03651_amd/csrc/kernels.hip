@@ -1184,14 +1184,25 @@ __global__ __launch_bounds__(kPfThreads, 8 / kPfWaves) void prefill_kernel(Prefi
 }
 
 // -------------------------------------------------------------------- merge
+//
+// One wave per (merged token, 4 query heads): 16 lanes per head, each lane
+// owning D/16 consecutive elements of the head's output row.  A 16-lane group
+// takes its entries 16 at a time (one per lane: slot and lse loaded in
+// parallel), rescales its running sums to the new maximum, then adds the
+// entries' partial rows, four independent loads at a time.
 
 template <int D>
 __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
+    constexpr int PER = D / 16;   // floats per lane
+    constexpr int NV = PER / 4;   // 16-byte loads per lane and partial row
     const int lane = threadIdx.x & 63;
+    const int c16 = lane & 15, base = lane & 48;
     const int64_t m = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
     if (m >= a.n_waves) return;
-    const int row = (int)(m / a.num_q_heads);
-    const int h = (int)(m - (int64_t)row * a.num_q_heads);
+    const int hgroups = (a.num_q_heads + 3) / 4;
+    const int row = (int)(m / hgroups);
+    const int h = 4 * (int)(m - (int64_t)row * hgroups) + (lane >> 4);
+    const bool hok = h < a.num_q_heads;
     const int tok = a.merge_tok[row];
     const int e0 = a.merge_ptr[row], e1 = a.merge_ptr[row + 1];
     // where head h of a slice's query i lands inside a descriptor's slots
@@ -1200,80 +1211,65 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     const int jh = h - kvh * a.group - hc * 16;
     const int nh = min(a.heads_per_chunk, a.group - hc * 16);
     const int rem = kvh * a.head_chunks + hc;
-    constexpr int PER = D / 64;
-    float acc[PER];
+    f32x4_t acc[NV];
 #pragma unroll
-    for (int k = 0; k < PER; ++k) acc[k] = 0.f;
+    for (int k = 0; k < NV; ++k) acc[k] = (f32x4_t){0.f, 0.f, 0.f, 0.f};
     float mx = -INFINITY, wsum = 0.f;
-    // entries 64 at a time, one per lane: slot and lse in parallel, then the
-    // partial rows in a loop whose loads do not depend on each other
-    for (int eb = e0; eb < e1; eb += 64) {
-        const int e = eb + lane;
-        int slot = 0;
+    for (int eb = e0; eb < e1; eb += 16) {
+        const int e = eb + c16;
+        int slot = 0;   // entries past the end (and heads past Hq) read slot 0 with weight 0
         float lse = -INFINITY;
-        if (e < e1) {
+        if (hok && e < e1) {
             const int part = a.merge_ent[2 * e], sh = a.merge_ent[2 * e + 1];
             slot = part + rem * (sh & 0x3FF) * a.heads_per_chunk + (sh >> 10) * nh + jh;
             lse = a.part_lse[slot];
         }
         float bm = lse;
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) bm = fmaxf(bm, __shfl_xor(bm, off));
+        for (int off = 8; off >= 1; off >>= 1) bm = fmaxf(bm, __shfl_xor(bm, off));
         const float m_new = fmaxf(mx, bm);
-        if (m_new == -INFINITY) continue;
-        const float alpha = exp2f(mx - m_new);   // 0 on the first batch
-        wsum *= alpha;
-#pragma unroll
-        for (int k = 0; k < PER; ++k) acc[k] *= alpha;
-        mx = m_new;
-        const float w = lse == -INFINITY ? 0.f : exp2f(lse - mx);
+        const float m_use = m_new == -INFINITY ? 0.f : m_new;
+        const float alpha = exp2f(mx - m_use);   // 0 while mx is -inf
+        const float w = lse == -INFINITY ? 0.f : exp2f(lse - m_use);
         float ws = w;
 #pragma unroll
-        for (int off = 32; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
-        wsum += ws;
-        const int n = min(64, e1 - eb);
-        // four partial rows per step, their loads independent of each other
-        auto row = [&](int i, float (&v)[PER]) {
-            const int si = __builtin_amdgcn_readlane(slot, i);
-            const float *po = a.part_o + (int64_t)si * D + lane * PER;
-            if constexpr (PER == 2) {
-                const float2 x = *(const float2 *)po;
-                v[0] = x.x;
-                v[1] = x.y;
-            } else {
-                v[0] = po[0];
-            }
-        };
-        auto add = [&](int i, const float (&v)[PER]) {
-            const float wi = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(w), i));
+        for (int off = 8; off >= 1; off >>= 1) ws += __shfl_xor(ws, off);
+        wsum = wsum * alpha + ws;
 #pragma unroll
-            for (int k = 0; k < PER; ++k) acc[k] += wi * v[k];
+        for (int k = 0; k < NV; ++k) acc[k] *= alpha;
+        mx = m_new;
+        const int n = min(16, e1 - eb);
+        auto load = [&](int i, f32x4_t (&v)[NV], float &wi) {
+            const int si = __shfl(slot, base + i);
+            wi = __shfl(w, base + i);
+            const f32x4_t *po = (const f32x4_t *)(a.part_o + (int64_t)si * D + c16 * PER);
+#pragma unroll
+            for (int k = 0; k < NV; ++k) v[k] = po[k];
         };
         int i = 0;
         for (; i + 4 <= n; i += 4) {
-            float v0[PER], v1[PER], v2[PER], v3[PER];
-            row(i, v0);
-            row(i + 1, v1);
-            row(i + 2, v2);
-            row(i + 3, v3);
-            add(i, v0);
-            add(i + 1, v1);
-            add(i + 2, v2);
-            add(i + 3, v3);
+            f32x4_t v[4][NV];
+            float wi[4];
+#pragma unroll
+            for (int j = 0; j < 4; ++j) load(i + j, v[j], wi[j]);
+#pragma unroll
+            for (int j = 0; j < 4; ++j)
+#pragma unroll
+                for (int k = 0; k < NV; ++k) acc[k] += wi[j] * v[j][k];
         }
         for (; i < n; ++i) {
-            float v0[PER];
-            row(i, v0);
-            add(i, v0);
+            f32x4_t v[NV];
+            float wi;
+            load(i, v, wi);
+#pragma unroll
+            for (int k = 0; k < NV; ++k) acc[k] += wi * v[k];
         }
     }
+    if (!hok) return;
     const float inv = wsum > 0.f ? 1.f / wsum : 0.f;
-    float *o = a.out + ((int64_t)tok * a.num_q_heads + h) * D + lane * PER;
-    if constexpr (PER == 2) {
-        *(float2 *)o = make_float2(acc[0] * inv, acc[1] * inv);
-    } else {
-        o[0] = acc[0] * inv;
-    }
+    f32x4_t *o = (f32x4_t *)(a.out + ((int64_t)tok * a.num_q_heads + h) * D + c16 * PER);
+#pragma unroll
+    for (int k = 0; k < NV; ++k) o[k] = acc[k] * inv;
 }
 
 // ------------------------------------------------------------- plan upload

@@ -64,10 +64,10 @@ struct PrefillArgs {
 };
 
 struct MergeArgs {
-    int64_t n_waves;                // merged rows * Hq
+    int64_t n_waves;                // merged rows * ceil(Hq / 4)
     int32_t num_q_heads, head_chunks, heads_per_chunk, group;
     const int32_t *merge_tok, *merge_ptr;
-    const int32_t *merge_ent;       // per entry: first slot of its descriptor, nt | i << 8
+    const int32_t *merge_ent;       // per entry: first slot of its descriptor, nt | i << 10
     const float *part_o, *part_lse;
     float *out;
 };
