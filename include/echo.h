@@ -15,7 +15,10 @@
  *     memory on the current HIP device.  All buffers belong to the caller and
  *     must outlive the work enqueued on `stream` (a hipStream_t, NULL for the
  *     default stream).  Calls return after enqueueing; they do not
- *     synchronise.
+ *     synchronise and allocate no device or pinned host memory; nothing a
+ *     call leaves behind affects a later call (per-thread host buffers for
+ *     validation and planning are reused, and echo_profile's opt-in events
+ *     are kept per thread).
  *   - Validation happens before anything is enqueued: a call that returns an
  *     error has enqueued nothing and changed nothing.
  *   - Return values are echo_status_t codes (0 on success, negative on error);
@@ -78,9 +81,11 @@ typedef struct {
 
 /* The rows of one iteration (Section 2.1: decode batching and chunked
  * prefill in one batch).  Device arrays, plus optional host mirrors with the
- * same contents.  The mirrors enable full validation (block ranges, aliased
- * writes) and are required by echo_attn_mixed, whose work plan (prefix
- * groups, key splits) is built on the host. */
+ * same contents.  With the mirrors, validation is complete (block ranges,
+ * aliased writes) and echo_attn_mixed plans on the host, grouping the rows
+ * that share prefix blocks (Section 6) so that those blocks are read once.
+ * Without them only the scalar fields are checked on the host and
+ * echo_attn_mixed builds a plan without prefix grouping on the device. */
 typedef struct {
     int32_t num_rows;             /* B */
     int32_t max_blocks_per_row;   /* row stride of block_tables */
@@ -118,21 +123,51 @@ int echo_kv_append(const echo_kv_pool_t *pool, const echo_batch_t *batch, const 
  *   out[t][h] = sum_{j<=p} softmax_j(sm_scale * q[t][h] . K_r[j][g]) V_r[j][g],
  * with g = h / (num_q_heads / num_kv_heads) and K_r/V_r the row's logical
  * sequence read through its block table.  Run echo_kv_append for the same
- * iteration first: attention reads the new tokens from the pool.  Blocks
- * that several decode rows share are read once per KV head for all of them.
+ * iteration first: attention reads the new tokens from the pool.
  * q: bf16 [T][num_q_heads][head_dim]; out: fp32 [T][num_q_heads][head_dim].
  * sm_scale must be positive and finite (ECHO_E_INVALID otherwise).
  * workspace: device scratch of at least echo_attn_workspace_bytes() bytes,
- * 256-byte aligned, not used concurrently by another call.  Host mirrors
- * are required (ECHO_E_INVALID without them). */
+ * 256-byte aligned, not used by another call until this call's work on
+ * `stream` has completed (calls on one stream may share it).
+ *
+ * Two planning modes, chosen by the host mirrors:
+ *   - with mirrors, the work plan is built on the host: decode rows whose
+ *     leading full blocks are the same physical blocks are grouped and those
+ *     blocks are read once per KV head for all of them; long key ranges are
+ *     split and prefill tiles balanced.  The plan is packed into
+ *     host_workspace -- pinned host memory the device reads coherently
+ *     (hipHostMalloc with hipHostMallocMapped | hipHostMallocCoherent), at
+ *     least echo_attn_host_workspace_bytes() bytes, 16-byte aligned -- and
+ *     copied into `workspace` by a kernel on `stream`.  The call does not
+ *     wait for that copy: the caller must not change or reuse host_workspace
+ *     until this call's work on `stream` has run past it (for example, wait
+ *     on an event recorded after the call, or rotate several buffers).
+ *     Memory that is not pinned host memory returns ECHO_E_WORKSPACE;
+ *   - without mirrors, host_workspace is ignored (may be NULL) and two small
+ *     kernels build the plan in `workspace` from the device metadata: no
+ *     prefix grouping (shared blocks are read once per row), decode rows cut
+ *     into equal key pieces, prefill rows into tiles, grids sized from the
+ *     scalar fields.  The results are the same within rounding.  Rows whose
+ *     metadata is inconsistent (the checks the mirrors would have run) get
+ *     no work and leave their outputs unchanged; nothing is read outside the
+ *     buffers described by the scalar fields.
+ * All checks run before anything is enqueued; a HIP launch failure (ECHO_E_HIP)
+ * can leave the kernels launched before it enqueued. */
 int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
                     int32_t num_q_heads, float sm_scale, float *out, void *workspace,
-                    size_t workspace_bytes, void *stream);
+                    size_t workspace_bytes, void *host_workspace, size_t host_workspace_bytes,
+                    void *stream);
 
-/* Workspace bytes echo_attn_mixed needs for this batch (from the host
- * mirrors), or 0 if the arguments are invalid. */
+/* Device workspace bytes echo_attn_mixed needs for this batch (the planning
+ * mode follows from the host mirrors; without them the size is a bound from
+ * the scalar fields), or 0 if the arguments are invalid. */
 size_t echo_attn_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
                                  int32_t num_q_heads);
+
+/* Pinned host workspace bytes echo_attn_mixed needs (the packed plan): 0
+ * without host mirrors, or when the arguments are invalid. */
+size_t echo_attn_host_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                                      int32_t num_q_heads);
 
 /* Block copy (copy-on-write of blocks that prefix-sharing rows alias; the
  * paper's automatic prefix caching, Section 6, implies it).  For each pair
@@ -212,7 +247,8 @@ int echo_validate(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t
  * plan upload and each kernel launch.  Recording is off unless enabled with
  * echo_profile(1) on the same thread; kernels not launched report 0. */
 typedef struct {
-    float upload_ms;    /* plan upload (a kernel copies it from pinned host memory) */
+    float upload_ms;    /* plan upload from the host workspace, or the two device
+                           planning kernels when there are no host mirrors */
     float prefill_ms;   /* prefill_kernel: chunked-prefill tiles */
     float decode_ms;    /* attn_kernel: decode split-KV / shared-prefix items */
     float merge_ms;     /* merge_kernel: log-sum-exp merge of partial results */

@@ -22,9 +22,12 @@
  * rows, then key rows, then value rows), w_o [H][Hq D], w_gate_up [2 I][H]
  * (gate rows, then up rows), w_down [H][I]; norms [H].
  *
- * The pool and batch follow echo.h (host mirrors required).  hidden [T][H]
- * bf16 is read and overwritten with the layer's output; all other buffers come
- * from the caller's workspace (echo_layer_workspace_bytes, 256-byte aligned).
+ * The pool and batch follow echo.h.  hidden [T][H] bf16 is read and
+ * overwritten with the layer's output; all other device buffers come from the
+ * caller's workspace (echo_layer_workspace_bytes, 256-byte aligned), and the
+ * attention's plan goes through host_workspace exactly as in
+ * echo_attn_mixed (echo_attn_host_workspace_bytes; not used, and may be
+ * NULL, without host mirrors).
  * The GEMMs run through hipBLASLt on `stream`, with a handle per host thread
  * and device created on first use.
  */
@@ -61,7 +64,8 @@ size_t echo_layer_workspace_bytes(const echo_layer_t *layer, const echo_kv_pool_
  * hidden and the pool then undefined. */
 int echo_layer_forward(const echo_layer_t *layer, const echo_kv_pool_t *pool,
                        const echo_batch_t *batch, void *hidden, void *workspace,
-                       size_t workspace_bytes, void *stream);
+                       size_t workspace_bytes, void *host_workspace,
+                       size_t host_workspace_bytes, void *stream);
 
 /* Per-stage GPU times of the calling thread's last echo_layer_forward while
  * echo_profile(1) is on: norms, qkv GEMM, RoPE, append, attention, o GEMM,

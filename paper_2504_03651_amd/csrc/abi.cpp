@@ -8,7 +8,6 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
-#include <mutex>
 #include <string>
 #include <vector>
 
@@ -228,23 +227,6 @@ int run_log2_for(int32_t sibling_waves) {
     return l;
 }
 
-// Pinned host staging for plan uploads: a small ring per device, each slot
-// guarded by an event so that a buffer is refilled only after the kernel
-// that copies it to the workspace has completed.
-struct StagingSlot {
-    void *host = nullptr;
-    void *dev = nullptr;   // the same memory as the device sees it
-    size_t cap = 0;
-    hipEvent_t ev = nullptr;
-    bool pending = false;
-};
-struct Staging {
-    std::mutex mu;
-    StagingSlot slots[4];
-    int next = 0;
-};
-Staging g_staging[64];
-
 // Opt-in per-kernel timing (echo_profile / echo_attn_timing).
 struct Profile {
     bool on = false;
@@ -281,44 +263,264 @@ int profile_events(hipEvent_t **out) {
     return ECHO_OK;
 }
 
-int upload_plan(const Plan &plan, void *workspace, hipStream_t stream) {
-    int dev = 0;
-    hipError_t e = hipGetDevice(&dev);
-    if (e != hipSuccess) return hip_fail(e, "hipGetDevice");
-    if (dev < 0 || dev >= 64) return fail(ECHO_E_HIP, "device index %d", dev);
-    Staging &st = g_staging[dev];
-    std::lock_guard<std::mutex> lock(st.mu);
-    StagingSlot &s = st.slots[st.next];
-    st.next = (st.next + 1) % 4;
-    if (!s.ev) {
-        e = hipEventCreateWithFlags(&s.ev, hipEventDisableTiming);
-        if (e != hipSuccess) return hip_fail(e, "hipEventCreate");
+// The plan goes to the device through the caller's pinned host workspace:
+// packed there on the host, then copied into the device workspace by a
+// kernel on the caller's stream.  The caller keeps the host workspace
+// untouched until that kernel has run (it is read on the device, not here).
+int check_host_workspace(void *host_ws, size_t bytes, size_t need, void **dev_ptr) {
+    if (!host_ws || bytes < need)
+        return fail(ECHO_E_WORKSPACE, "host workspace of %zu bytes, need %zu", bytes, need);
+    if (((uintptr_t)host_ws & 15u) != 0)
+        return fail(ECHO_E_WORKSPACE, "host workspace must be 16-byte aligned");
+    hipError_t e = hipHostGetDevicePointer(dev_ptr, host_ws, 0);
+    if (e != hipSuccess) {
+        (void)hipGetLastError();
+        return fail(ECHO_E_WORKSPACE, "host workspace is not pinned host memory mapped for the "
+                                      "device (%s)", hipGetErrorString(e));
     }
-    if (s.pending) {
-        e = hipEventSynchronize(s.ev);
-        if (e != hipSuccess) return hip_fail(e, "hipEventSynchronize");
-        s.pending = false;
-    }
-    const size_t bytes = (size_t)plan.layout.upload_words * 4;
-    if (s.cap < bytes) {
-        if (s.host) (void)hipHostFree(s.host);
-        s.host = s.dev = nullptr;
-        s.cap = 0;
-        const size_t cap = std::max<size_t>(bytes + bytes / 2, 1 << 20);
-        // coherent: the upload kernel reads what the host wrote, uncached
-        e = hipHostMalloc(&s.host, cap, hipHostMallocMapped | hipHostMallocCoherent);
-        if (e != hipSuccess) return hip_fail(e, "hipHostMalloc (plan staging)");
-        e = hipHostGetDevicePointer(&s.dev, s.host, 0);
-        if (e != hipSuccess) return hip_fail(e, "hipHostGetDevicePointer (plan staging)");
-        s.cap = cap;
-    }
-    pack_plan(plan, s.host);
-    e = launch_plan_upload(s.dev, workspace, plan.layout.upload_words, stream);
-    if (e != hipSuccess) return hip_fail(e, "plan upload launch");
-    e = hipEventRecord(s.ev, stream);
-    if (e != hipSuccess) return hip_fail(e, "hipEventRecord");
-    s.pending = true;
     return ECHO_OK;
+}
+
+// Scalar bounds of the device-built plan for a batch without host mirrors.
+struct DevLayout {
+    int32_t split_keys = 0, tile_tokens = 0, slots_per_desc = 0, head_chunks = 1,
+            heads_per_chunk = 1, waves_per_desc = 1, pf_max_blocks = 0;
+    int64_t cap_desc = 0, cap_pdesc = 0, cap_mrows = 0, cap_ent = 0, cap_slots = 0;
+    int64_t off_row_info = 0, off_desc = 0, off_pdesc = 0, off_mtok = 0, off_mptr = 0,
+            off_ment = 0, off_lse = 0, off_o = 0, total_words = 0;
+};
+
+int64_t align_up(int64_t w, int64_t a) { return (w + a - 1) / a * a; }
+
+int dev_layout(const echo_kv_pool_t *pool, const echo_batch_t *b, int32_t Hq, DevLayout &L) {
+    const int64_t B = b->num_rows, Hkv = pool->num_kv_heads, G = Hq / Hkv;
+    L.heads_per_chunk = (int32_t)std::min<int64_t>(G, kWaveQueries);
+    L.head_chunks = (int32_t)((G + kWaveQueries - 1) / kWaveQueries);
+    L.waves_per_desc = (int32_t)(Hkv * L.head_chunks);
+    L.slots_per_desc = L.waves_per_desc * L.heads_per_chunk;
+    // decode pieces: the host planner's rule, with every row taken at the
+    // longest length the scalars allow
+    const PlanOptions o = plan_options(pool);
+    const int64_t seg_blocks = B * (((int64_t)b->max_seq_len + kBlock - 1) / kBlock);
+    const int64_t split = std::max<int64_t>(
+        std::min(kMinSplitBlocks, std::max(2, o.split_blocks)),
+        std::min<int64_t>(o.split_blocks, seg_blocks * Hkv * L.head_chunks / kSplitTargetUnits));
+    L.split_keys = (int32_t)(split * kBlock);
+    L.tile_tokens = (int32_t)std::max<int64_t>(1, kPrefillQueries / G);
+    const int64_t P = ((int64_t)b->max_seq_len + L.split_keys - 1) / L.split_keys;
+    L.cap_desc = B * P;
+    L.cap_ent = B * P;
+    L.cap_mrows = B;
+    L.cap_slots = B * P * L.slots_per_desc;
+    L.cap_pdesc = std::min(B * (((int64_t)b->max_q_len + L.tile_tokens - 1) / L.tile_tokens),
+                           ((int64_t)b->num_tokens + L.tile_tokens - 1) / L.tile_tokens + B);
+    if (L.cap_desc * L.waves_per_desc > ((int64_t)1 << 31) - (1 << 20) ||
+        L.cap_pdesc * Hkv > ((int64_t)1 << 31) - (1 << 20) || L.cap_slots > ((int64_t)1 << 31) - 1)
+        return fail(ECHO_E_UNSUPPORTED, "batch too large for a plan built on the device");
+    L.pf_max_blocks = (int32_t)std::min<int64_t>(((int64_t)b->max_seq_len + kBlock - 1) / kBlock,
+                                                 prefill_max_blocks(pool->head_dim));
+    int64_t w = kHdrWords;
+    L.off_row_info = w;  w = align_up(w + B, 8);
+    L.off_desc = w;      w += L.cap_desc * (int64_t)(sizeof(WorkDesc) / 4);
+    L.off_pdesc = w;     w += L.cap_pdesc * (int64_t)(sizeof(PrefillDesc) / 4);
+    L.off_mtok = w;      w += L.cap_mrows;
+    L.off_mptr = w;      w += L.cap_mrows + 1;
+    L.off_ment = w;      w += 2 * L.cap_ent;
+    w = align_up(w, 64);
+    L.off_lse = w;       w += L.cap_slots;
+    w = align_up(w, 64);
+    L.off_o = w;         w += L.cap_slots * pool->head_dim;
+    L.total_words = align_up(w, 64);
+    return ECHO_OK;
+}
+
+// Everything echo_attn_mixed launches after the plan is in the workspace.
+struct AttnLaunch {
+    const WorkDesc *desc = nullptr;
+    const PrefillDesc *pdesc = nullptr;
+    const int32_t *tok_list = nullptr, *klim = nullptr, *merge_tok = nullptr,
+                  *merge_ptr = nullptr, *merge_ent = nullptr, *counts = nullptr;
+    float *part_lse = nullptr, *part_o = nullptr;
+    int64_t n_desc = 0, n_merge_rows = 0;
+    int32_t n_pdesc_grid = 0;     // prefill descriptors that get workgroups (a capacity with counts)
+    int32_t head_chunks = 1, heads_per_chunk = 1, waves_per_desc = 1, run_log2 = 0,
+            pf_max_blocks = 0;
+};
+
+int launch_attention(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
+                     int32_t num_q_heads, float sm_scale, float *out, const AttnLaunch &w,
+                     hipStream_t s, hipEvent_t *ev) {
+    AttnArgs a;
+    a.desc = w.desc;
+    a.n_waves = w.n_desc * w.waves_per_desc;
+    a.waves_per_desc = w.waves_per_desc;
+    a.run_log2 = w.run_log2;
+    a.head_chunks = w.head_chunks;
+    a.heads_per_chunk = w.heads_per_chunk;
+    a.group = num_q_heads / pool->num_kv_heads;
+    a.tok_list = w.tok_list;
+    a.klim = w.klim;
+    a.q = (const uint16_t *)q;
+    a.num_q_heads = num_q_heads;
+    a.num_kv_heads = pool->num_kv_heads;
+    a.k = pool->k;
+    a.v = pool->v;
+    a.k_scale = pool->k_scale;
+    a.v_scale = pool->v_scale;
+    a.block_tables = batch->block_tables;
+    a.max_blocks_per_row = batch->max_blocks_per_row;
+    a.scale_log2 = (float)((double)sm_scale * 1.4426950408889634);
+    a.out = out;
+    a.part_o = w.part_o;
+    a.part_lse = w.part_lse;
+    a.counts = w.counts;
+    MergeArgs m;
+    m.n_waves = w.n_merge_rows * ((num_q_heads + 3) / 4);
+    m.counts = w.counts;
+    m.num_q_heads = num_q_heads;
+    m.head_chunks = w.head_chunks;
+    m.heads_per_chunk = w.heads_per_chunk;
+    m.group = a.group;
+    m.merge_tok = w.merge_tok;
+    m.merge_ptr = w.merge_ptr;
+    m.merge_ent = w.merge_ent;
+    m.part_o = a.part_o;
+    m.part_lse = a.part_lse;
+    m.out = out;
+    PrefillArgs pf;
+    pf.pdesc = w.pdesc;
+    pf.n_pdesc = w.n_pdesc_grid;   // chained descriptors follow these
+    pf.n_logical = (int32_t)((int64_t)w.n_pdesc_grid * pool->num_kv_heads);
+    pf.per_xcd = (pf.n_logical + 7) / 8;
+    pf.group = a.group;
+    pf.seq_lens = batch->seq_lens;
+    pf.q_start = batch->q_start;
+    pf.counts = w.counts;
+    pf.q = a.q;
+    pf.num_q_heads = num_q_heads;
+    pf.num_kv_heads = pool->num_kv_heads;
+    pf.k = pool->k;
+    pf.v = pool->v;
+    pf.k_scale = pool->k_scale;
+    pf.v_scale = pool->v_scale;
+    pf.block_tables = batch->block_tables;
+    pf.max_blocks_per_row = batch->max_blocks_per_row;
+    pf.scale_log2 = a.scale_log2;
+    pf.out = out;
+    pf.max_blocks = w.pf_max_blocks;
+    pf.head_chunks = w.head_chunks;
+    pf.heads_per_chunk = w.heads_per_chunk;
+    pf.part_o = a.part_o;
+    pf.part_lse = a.part_lse;
+    const int D = pool->head_dim;
+    const bool fp8 = pool->dtype == ECHO_KV_FP8_E4M3;
+    hipError_t e;
+    // prefill, decode and merge in that order on the caller's stream; with
+    // profiling on, an event pair around each kernel that launches (an empty
+    // pair still costs GPU time between the two records)
+    if (pf.n_logical > 0) {
+        if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_prefill(pf, D, fp8, s)) != hipSuccess) return hip_fail(e, "prefill launch");
+        if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    if (a.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[4], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_decode(a, D, fp8, s)) != hipSuccess) return hip_fail(e, "decode launch");
+        if (ev && (e = hipEventRecord(ev[5], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    if (m.n_waves > 0) {
+        if (ev && (e = hipEventRecord(ev[6], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+        if ((e = launch_merge(m, D, s)) != hipSuccess) return hip_fail(e, "merge launch");
+        if (ev && (e = hipEventRecord(ev[7], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    }
+    g_prof.valid = ev != nullptr;
+    g_prof.launched[0] = true;
+    g_prof.launched[1] = pf.n_logical > 0;
+    g_prof.launched[2] = a.n_waves > 0;
+    g_prof.launched[3] = m.n_waves > 0;
+    return ECHO_OK;
+}
+
+// Checks shared by both planning modes.
+int check_attn_args(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32_t num_q_heads) {
+    int rc = check_pool(pool);
+    if (rc) return rc;
+    rc = check_batch(pool, batch, false);
+    if (rc) return rc;
+    if (num_q_heads <= 0 || num_q_heads % pool->num_kv_heads != 0)
+        return fail(ECHO_E_INVALID, "num_q_heads %d is not a multiple of num_kv_heads %d",
+                    num_q_heads, pool->num_kv_heads);
+    if (num_q_heads / pool->num_kv_heads > kPrefillQueries)
+        return fail(ECHO_E_UNSUPPORTED, "more than %d query heads per KV head", kPrefillQueries);
+    return ECHO_OK;
+}
+
+// The device-built plan (no host mirrors): two planning kernels, then the
+// attention kernels reading their counts from the plan's header.
+int attn_device_planned(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
+                        int32_t num_q_heads, float sm_scale, float *out, void *workspace,
+                        size_t workspace_bytes, hipStream_t s) {
+    DevLayout L;
+    int rc = dev_layout(pool, batch, num_q_heads, L);
+    if (rc) return rc;
+    const size_t need = (size_t)L.total_words * 4;
+    if (!workspace || workspace_bytes < need)
+        return fail(ECHO_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0)
+        return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
+    hipEvent_t *ev = nullptr;
+    rc = profile_events(&ev);
+    if (rc) return rc;
+    g_prof.valid = false;
+    int32_t *w = (int32_t *)workspace;
+    DevPlanArgs d;
+    d.block_tables = batch->block_tables;
+    d.seq_lens = batch->seq_lens;
+    d.q_start = batch->q_start;
+    d.row_kind = batch->row_kind;
+    d.num_rows = batch->num_rows;
+    d.num_tokens = batch->num_tokens;
+    d.max_blocks_per_row = batch->max_blocks_per_row;
+    d.num_blocks = pool->num_blocks;
+    d.max_seq_len = batch->max_seq_len;
+    d.split_keys = L.split_keys;
+    d.tile_tokens = L.tile_tokens;
+    d.slots_per_desc = L.slots_per_desc;
+    d.prefill_max_keys = prefill_max_blocks(pool->head_dim) * kBlock;
+    d.cap_desc = L.cap_desc;
+    d.cap_pdesc = L.cap_pdesc;
+    d.cap_merge_rows = L.cap_mrows;
+    d.cap_ent = L.cap_ent;
+    d.cap_slots = L.cap_slots;
+    d.row_info = w + L.off_row_info;
+    d.hdr = w;
+    d.desc = (WorkDesc *)(w + L.off_desc);
+    d.pdesc = (PrefillDesc *)(w + L.off_pdesc);
+    d.merge_tok = w + L.off_mtok;
+    d.merge_ptr = w + L.off_mptr;
+    d.merge_ent = w + L.off_ment;
+    hipError_t e;
+    if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = launch_dev_plan(d, s)) != hipSuccess) return hip_fail(e, "device plan launch");
+    if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    AttnLaunch a;
+    a.desc = d.desc;
+    a.pdesc = d.pdesc;
+    a.merge_tok = d.merge_tok;
+    a.merge_ptr = d.merge_ptr;
+    a.merge_ent = d.merge_ent;
+    a.counts = w;
+    a.part_lse = (float *)(w + L.off_lse);
+    a.part_o = (float *)(w + L.off_o);
+    a.n_desc = L.cap_desc;
+    a.n_merge_rows = L.cap_mrows;
+    a.n_pdesc_grid = (int32_t)L.cap_pdesc;
+    a.head_chunks = L.head_chunks;
+    a.heads_per_chunk = L.heads_per_chunk;
+    a.waves_per_desc = L.waves_per_desc;
+    a.run_log2 = 0;
+    a.pf_max_blocks = L.pf_max_blocks;
+    return launch_attention(pool, batch, q, num_q_heads, sm_scale, out, a, s, ev);
 }
 
 }  // namespace
@@ -461,9 +663,26 @@ int echo_block_copy(const echo_kv_pool_t *pool, const int32_t *pairs, int32_t n_
 size_t echo_attn_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
                                  int32_t num_q_heads) {
     g_error.clear();
+    if (check_attn_args(pool, batch, num_q_heads) != ECHO_OK) return 0;
+    if (batch->num_rows == 0) return 256;
+    if (!has_mirrors(batch)) {
+        DevLayout L;
+        if (dev_layout(pool, batch, num_q_heads, L) != ECHO_OK) return 0;
+        return (size_t)L.total_words * 4;
+    }
     thread_local Plan plan;
     if (plan_for(pool, batch, num_q_heads, plan) != ECHO_OK) return 0;
     return (size_t)plan.layout.total_words * 4;
+}
+
+size_t echo_attn_host_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
+                                      int32_t num_q_heads) {
+    g_error.clear();
+    if (check_attn_args(pool, batch, num_q_heads) != ECHO_OK) return 0;
+    if (batch->num_rows == 0 || !has_mirrors(batch)) return 0;
+    thread_local Plan plan;
+    if (plan_for(pool, batch, num_q_heads, plan) != ECHO_OK) return 0;
+    return (size_t)plan.layout.upload_words * 4;
 }
 
 int echo_attn_plan_stats(const echo_kv_pool_t *pool, const echo_batch_t *batch,
@@ -538,129 +757,71 @@ int echo_attn_plan_pack(const echo_kv_pool_t *pool, const echo_batch_t *batch,
 
 int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
                     int32_t num_q_heads, float sm_scale, float *out, void *workspace,
-                    size_t workspace_bytes, void *stream) {
+                    size_t workspace_bytes, void *host_workspace, size_t host_workspace_bytes,
+                    void *stream) {
     g_error.clear();
-    thread_local Plan plan;
-    int rc = plan_for(pool, batch, num_q_heads, plan);
+    int rc = check_attn_args(pool, batch, num_q_heads);
     if (rc) return rc;
     if (batch->num_rows == 0) return ECHO_OK;
     if (!q || !out) return fail(ECHO_E_INVALID, "q / out is NULL");
     if (!(sm_scale > 0.f) || !std::isfinite(sm_scale))
         return fail(ECHO_E_INVALID, "sm_scale must be positive and finite");
-    const size_t need = (size_t)plan.layout.total_words * 4;
-    if (!workspace || workspace_bytes < need)
-        return fail(ECHO_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
-    if (((uintptr_t)workspace & 255u) != 0)
-        return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
+    hipStream_t s = (hipStream_t)stream;
+    if (!has_mirrors(batch))
+        return attn_device_planned(pool, batch, q, num_q_heads, sm_scale, out, workspace,
+                                   workspace_bytes, s);
+
+    thread_local Plan plan;
+    rc = plan_for(pool, batch, num_q_heads, plan);
+    if (rc) return rc;
+    const PlanLayout &L = plan.layout;
     int32_t pf_blocks = 0;
     for (const PrefillDesc &d : plan.pdesc)
         pf_blocks = std::max(pf_blocks, (d.key_end + kBlock - 1) / kBlock - d.key_begin / kBlock);
     if (pf_blocks > prefill_max_blocks(pool->head_dim))
         return fail(ECHO_E_UNSUPPORTED, "prefill row of %d blocks exceeds the %d-block limit",
                     pf_blocks, prefill_max_blocks(pool->head_dim));
-    hipStream_t s = (hipStream_t)stream;
+    const size_t need = (size_t)L.total_words * 4;
+    if (!workspace || workspace_bytes < need)
+        return fail(ECHO_E_WORKSPACE, "workspace of %zu bytes, need %zu", workspace_bytes, need);
+    if (((uintptr_t)workspace & 255u) != 0)
+        return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
+    void *staged = nullptr;
+    rc = check_host_workspace(host_workspace, host_workspace_bytes, (size_t)L.upload_words * 4,
+                              &staged);
+    if (rc) return rc;
     hipEvent_t *ev = nullptr;
     rc = profile_events(&ev);
     if (rc) return rc;
     g_prof.valid = false;
-    if (ev) {
-        hipError_t e0 = hipEventRecord(ev[0], s);
-        if (e0 != hipSuccess) return hip_fail(e0, "hipEventRecord");
-    }
-    rc = upload_plan(plan, workspace, s);
-    if (rc) return rc;
-    if (ev) {
-        hipError_t e0 = hipEventRecord(ev[1], s);
-        if (e0 != hipSuccess) return hip_fail(e0, "hipEventRecord");
-    }
+    // every check is done: pack the plan into the host workspace and enqueue
+    pack_plan(plan, host_workspace);
+    hipError_t e;
+    if (ev && (e = hipEventRecord(ev[0], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
+    if ((e = launch_plan_upload(staged, workspace, L.upload_words, s)) != hipSuccess)
+        return hip_fail(e, "plan upload launch");
+    if (ev && (e = hipEventRecord(ev[1], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
 
-    const PlanLayout &L = plan.layout;
     int32_t *w = (int32_t *)workspace;
-    AttnArgs a;
+    AttnLaunch a;
     a.desc = (const WorkDesc *)(w + L.off_desc);
-    a.n_waves = L.n_desc * plan.waves_per_desc;
-    a.waves_per_desc = plan.waves_per_desc;
-    a.run_log2 = run_log2_for(plan.sibling_waves);
-    a.head_chunks = plan.head_chunks;
-    a.heads_per_chunk = plan.heads_per_chunk;
-    a.group = num_q_heads / pool->num_kv_heads;
+    a.pdesc = (const PrefillDesc *)(w + L.off_pdesc);
     a.tok_list = w + L.off_tok_list;
     a.klim = w + L.off_klim;
-    a.q = (const uint16_t *)q;
-    a.num_q_heads = num_q_heads;
-    a.num_kv_heads = pool->num_kv_heads;
-    a.k = pool->k;
-    a.v = pool->v;
-    a.k_scale = pool->k_scale;
-    a.v_scale = pool->v_scale;
-    a.block_tables = batch->block_tables;
-    a.max_blocks_per_row = batch->max_blocks_per_row;
-    a.scale_log2 = (float)((double)sm_scale * 1.4426950408889634);
-    a.out = out;
-    a.part_o = (float *)(w + L.off_part_o);
+    a.merge_tok = w + L.off_merge_tok;
+    a.merge_ptr = w + L.off_merge_ptr;
+    a.merge_ent = w + L.off_merge_ent;
     a.part_lse = (float *)(w + L.off_part_lse);
-    MergeArgs m;
-    m.n_waves = L.n_merge_rows * ((num_q_heads + 3) / 4);
-    m.num_q_heads = num_q_heads;
-    m.head_chunks = plan.head_chunks;
-    m.heads_per_chunk = plan.heads_per_chunk;
-    m.group = a.group;
-    m.merge_tok = w + L.off_merge_tok;
-    m.merge_ptr = w + L.off_merge_ptr;
-    m.merge_ent = w + L.off_merge_ent;
-    m.part_o = a.part_o;
-    m.part_lse = a.part_lse;
-    m.out = out;
-    PrefillArgs pf;
-    pf.pdesc = (const PrefillDesc *)(w + L.off_pdesc);
-    pf.n_pdesc = plan.pdesc_grid;   // chained descriptors follow these
-    pf.n_logical = (int32_t)((int64_t)plan.pdesc_grid * pool->num_kv_heads);
-    pf.per_xcd = (pf.n_logical + 7) / 8;
-    pf.group = a.group;
-    pf.klim = a.klim;
-    pf.q = a.q;
-    pf.num_q_heads = num_q_heads;
-    pf.num_kv_heads = pool->num_kv_heads;
-    pf.k = pool->k;
-    pf.v = pool->v;
-    pf.k_scale = pool->k_scale;
-    pf.v_scale = pool->v_scale;
-    pf.block_tables = batch->block_tables;
-    pf.max_blocks_per_row = batch->max_blocks_per_row;
-    pf.scale_log2 = a.scale_log2;
-    pf.out = out;
-    pf.max_blocks = pf_blocks;
-    pf.head_chunks = plan.head_chunks;
-    pf.heads_per_chunk = plan.heads_per_chunk;
-    pf.part_o = a.part_o;
-    pf.part_lse = a.part_lse;
-    const int D = pool->head_dim;
-    const bool fp8 = pool->dtype == ECHO_KV_FP8_E4M3;
-    hipError_t e;
-    // prefill, decode and merge in that order on the caller's stream; with
-    // profiling on, an event pair around each kernel that launches (an empty
-    // pair still costs GPU time between the two records)
-    if (pf.n_logical > 0) {
-        if (ev && (e = hipEventRecord(ev[2], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = launch_prefill(pf, D, fp8, s)) != hipSuccess) return hip_fail(e, "prefill launch");
-        if (ev && (e = hipEventRecord(ev[3], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    }
-    if (a.n_waves > 0) {
-        if (ev && (e = hipEventRecord(ev[4], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = launch_decode(a, D, fp8, s)) != hipSuccess) return hip_fail(e, "decode launch");
-        if (ev && (e = hipEventRecord(ev[5], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    }
-    if (m.n_waves > 0) {
-        if (ev && (e = hipEventRecord(ev[6], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-        if ((e = launch_merge(m, D, s)) != hipSuccess) return hip_fail(e, "merge launch");
-        if (ev && (e = hipEventRecord(ev[7], s)) != hipSuccess) return hip_fail(e, "hipEventRecord");
-    }
-    g_prof.valid = ev != nullptr;
-    g_prof.launched[0] = true;
-    g_prof.launched[1] = pf.n_logical > 0;
-    g_prof.launched[2] = a.n_waves > 0;
-    g_prof.launched[3] = m.n_waves > 0;
-    return ECHO_OK;
+    a.part_o = (float *)(w + L.off_part_o);
+    a.n_desc = L.n_desc;
+    a.n_merge_rows = L.n_merge_rows;
+    a.n_pdesc_grid = plan.pdesc_grid;
+    a.head_chunks = plan.head_chunks;
+    a.heads_per_chunk = plan.heads_per_chunk;
+    a.waves_per_desc = plan.waves_per_desc;
+    a.run_log2 = run_log2_for(plan.sibling_waves);
+    a.pf_max_blocks = pf_blocks;
+    return launch_attention(pool, batch, q, num_q_heads, sm_scale, out, a, s, ev);
 }
 
 }  // extern "C"

@@ -551,6 +551,7 @@ __device__ __forceinline__ void decode_body(const AttnArgs &a, int P, int tid) {
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int64_t idx = (int64_t)dec_logical(P, a.run_log2) * 4 + wave;
     if (idx >= a.n_waves) return;
+    if (a.counts && idx >= (int64_t)ro_load(a.counts, kHdrDesc) * a.waves_per_desc) return;
     const int di = (int)(idx / a.waves_per_desc);
     const int rem = (int)(idx - (int64_t)di * a.waves_per_desc);
     const int kvh = rem / a.head_chunks;
@@ -820,6 +821,9 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
     const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int g4 = lane >> 4, c16 = lane & 15;
     const int G = a.group;
+    // token t of the row sits at position t - (q_start[row + 1] - seq_lens[row])
+    // and sees the keys up to and including it
+    const int klim_base = __builtin_amdgcn_readfirstlane(a.seq_lens[row] - a.q_start[row + 1] + 1);
 
     // this lane's two query columns (N tiles nn = 0, 1)
     bf16x8_t qf[2][NC];
@@ -832,7 +836,7 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
         qok[nn] = tl < ntok;
         qtok[nn] = tok0 + (qok[nn] ? tl : 0);
         qhead[nn] = kvh * G + (qi - tl * G);
-        klim[nn] = qok[nn] ? a.klim[qtok[nn]] : 0;
+        klim[nn] = qok[nn] ? klim_base + qtok[nn] : 0;
         const uint16_t *qp = a.q + ((int64_t)qtok[nn] * a.num_q_heads + qhead[nn]) * D + 8 * g4;
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
@@ -1173,6 +1177,7 @@ __device__ __forceinline__ void prefill_body(const PrefillArgs &a, int P) {
     if (L >= a.n_logical) return;
     const int kvh = L / a.n_pdesc;
     int di = L - kvh * a.n_pdesc;
+    if (a.counts && di >= ro_load(a.counts, kHdrPdesc)) return;
     for (;;) {
         prefill_piece<D, FP8>(a, kvh, di);
         const int next = __builtin_amdgcn_readfirstlane(((const int32_t *)(a.pdesc + di))[7]);
@@ -1205,6 +1210,7 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     if (m >= a.n_waves) return;
     const int hgroups = (a.num_q_heads + 3) / 4;
     const int row = (int)(m / hgroups);
+    if (a.counts && row >= ro_load(a.counts, kHdrMergeRows)) return;
     const int h = 4 * (int)(m - (int64_t)row * hgroups) + (lane >> 4);
     const bool hok = h < a.num_q_heads;
     const int tok = a.merge_tok[row];
@@ -1274,6 +1280,166 @@ __global__ __launch_bounds__(256) void merge_kernel(MergeArgs a) {
     f32x4_t *o = (f32x4_t *)(a.out + ((int64_t)tok * a.num_q_heads + h) * D + c16 * PER);
 #pragma unroll
     for (int k = 0; k < NV; ++k) o[k] = acc[k] * inv;
+}
+
+// ------------------------------------------------------- device-built plan
+//
+// For batches given without host mirrors: the plan is built on the GPU from
+// the row metadata, with no prefix grouping.  Two kernels:
+//   dev_rows_kernel  one workgroup per row: checks the row's metadata and
+//                    block ids and records how many decode pieces or
+//                    prefill tiles it needs (-1: skipped)
+//   dev_plan_kernel  one workgroup: scans those counts and writes the
+//                    descriptors, merge lists and the header
+// Rows whose metadata is inconsistent (or that would not fit a region, which
+// only inconsistent q_start can cause) get no work and are counted in the
+// header, so every kernel after them stays inside its buffers.
+
+__global__ __launch_bounds__(256) void dev_rows_kernel(DevPlanArgs a) {
+    const int r = blockIdx.x;
+    const int t0 = a.q_start[r], t1 = a.q_start[r + 1];
+    const int q = t1 - t0, L = a.seq_lens[r], kind = a.row_kind[r];
+    bool ok = q >= 1 && L >= q && L <= a.max_seq_len && t0 >= 0 && t1 <= a.num_tokens &&
+              (kind == 0 ? q == 1 : kind == 1) && (kind == 0 || L <= a.prefill_max_keys);
+    const int nb = ok ? (L + 15) / 16 : 0;
+    const int32_t *bt = a.block_tables + (int64_t)r * a.max_blocks_per_row;
+    int bad = 0;
+    for (int j = threadIdx.x; j < nb; j += 256) {
+        const int id = bt[j];
+        bad |= (id < 0 || id >= a.num_blocks);
+    }
+    bad = __syncthreads_or(bad);
+    if (threadIdx.x == 0) {
+        int n = -1;
+        if (ok && !bad)
+            n = kind == 0 ? (L + a.split_keys - 1) / a.split_keys : (q + a.tile_tokens - 1) / a.tile_tokens;
+        a.row_info[r] = n;
+    }
+}
+
+// exclusive scan over the 1024 threads of one workgroup of NV values per
+// thread; returns the totals in tot[]
+template <int NV>
+__device__ __forceinline__ void scan1024(int64_t (&v)[NV], int64_t (&tot)[NV], int64_t (*wsum)[NV]) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    int64_t inc[NV];
+#pragma unroll
+    for (int k = 0; k < NV; ++k) inc[k] = v[k];
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1)
+#pragma unroll
+        for (int k = 0; k < NV; ++k) {
+            const int64_t y = __shfl_up(inc[k], off);
+            if (lane >= off) inc[k] += y;
+        }
+    if (lane == 63)
+#pragma unroll
+        for (int k = 0; k < NV; ++k) wsum[wave][k] = inc[k];
+    __syncthreads();
+#pragma unroll
+    for (int k = 0; k < NV; ++k) {
+        int64_t before = 0, all = 0;
+        for (int w = 0; w < 16; ++w) {
+            before += w < wave ? wsum[w][k] : 0;
+            all += wsum[w][k];
+        }
+        v[k] = before + inc[k] - v[k];
+        tot[k] = all;
+    }
+    __syncthreads();   // wsum is reused by the next call
+}
+
+__global__ __launch_bounds__(1024) void dev_plan_kernel(DevPlanArgs a) {
+    __shared__ int64_t wsum[16][5];
+    __shared__ unsigned long long used[5];   // end of the written part of each region
+    __shared__ int bad_rows;
+    if (threadIdx.x < 5) used[threadIdx.x] = 0;
+    if (threadIdx.x == 0) bad_rows = 0;
+    __syncthreads();
+    const int64_t cap[5] = {a.cap_desc, a.cap_pdesc, a.cap_merge_rows, a.cap_ent, a.cap_slots};
+    int64_t carry[5] = {0, 0, 0, 0, 0};
+    for (int base = 0; base < a.num_rows; base += 1024) {
+        const int r = base + (int)threadIdx.x;
+        int info = -2, kind = 0;
+        if (r < a.num_rows) {
+            info = a.row_info[r];
+            kind = a.row_kind[r];
+        }
+        const int dec = (info > 0 && kind == 0) ? info : 0;
+        const int pf = (info > 0 && kind == 1) ? info : 0;
+        // counts: decode pieces, prefill tiles, merged tokens, merge entries, slots
+        int64_t v[5] = {dec, pf, dec > 1 ? 1 : 0, dec > 1 ? dec : 0,
+                        dec > 1 ? (int64_t)dec * a.slots_per_desc : 0};
+        const int64_t n[5] = {v[0], v[1], v[2], v[3], v[4]};
+        int64_t tot[5];
+        scan1024<5>(v, tot, wsum);
+        int64_t off[5];
+        bool fits = true;
+#pragma unroll
+        for (int k = 0; k < 5; ++k) {
+            off[k] = carry[k] + v[k];
+            fits = fits && off[k] + n[k] <= cap[k];
+            carry[k] += tot[k];
+        }
+        if (r < a.num_rows && (info == -1 || !fits)) atomicAdd(&bad_rows, 1);
+        if (r < a.num_rows && fits && (dec > 0 || pf > 0)) {
+#pragma unroll
+            for (int k = 0; k < 5; ++k)
+                if (n[k] > 0) atomicMax(&used[k], (unsigned long long)(off[k] + n[k]));
+            const int t0 = a.q_start[r];
+            const int L = a.seq_lens[r];
+            for (int p = 0; p < dec; ++p) {
+                WorkDesc d;
+                d.tok_off = 0;
+                d.shape = 1;
+                d.bt_row = r;
+                d.key_begin = p * a.split_keys;
+                d.key_end = min((p + 1) * a.split_keys, L);
+                d.part = dec > 1 ? (int32_t)(off[4] + (int64_t)p * a.slots_per_desc) : -1;
+                d.tok1 = t0;
+                d.klim1 = L;
+                a.desc[off[0] + p] = d;
+            }
+            if (dec > 1) {
+                a.merge_tok[off[2]] = t0;
+                a.merge_ptr[off[2]] = (int32_t)off[3];
+                for (int p = 0; p < dec; ++p) {
+                    a.merge_ent[2 * (off[3] + p)] = (int32_t)(off[4] + (int64_t)p * a.slots_per_desc);
+                    a.merge_ent[2 * (off[3] + p) + 1] = 1;   // a one-token slice, query 0
+                }
+            }
+            const int q = a.q_start[r + 1] - t0, c = L - q;
+            for (int k = 0; k < pf; ++k) {   // the tile with the most keys first
+                const int kk = pf - 1 - k;
+                PrefillDesc d;
+                d.row = r;
+                d.tok0 = t0 + kk * a.tile_tokens;
+                d.ntok = min(a.tile_tokens, q - kk * a.tile_tokens);
+                d.key_end = c + kk * a.tile_tokens + d.ntok;
+                d.key_begin = 0;
+                d.part = -1;
+                d.kfull = d.key_end - d.ntok + 1;
+                d.next = 0;
+                a.pdesc[off[1] + k] = d;
+            }
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        a.hdr[kHdrDesc] = (int32_t)used[0];
+        a.hdr[kHdrPdesc] = (int32_t)used[1];
+        a.hdr[kHdrMergeRows] = (int32_t)used[2];
+        a.hdr[kHdrSlots] = (int32_t)used[4];
+        a.hdr[kHdrBadRows] = bad_rows;
+        a.merge_ptr[used[2]] = (int32_t)used[3];
+    }
+}
+
+hipError_t launch_dev_plan(const DevPlanArgs &a, hipStream_t s) {
+    if (a.num_rows <= 0) return hipSuccess;
+    hipLaunchKernelGGL(dev_rows_kernel, dim3((unsigned)a.num_rows), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(dev_plan_kernel, dim3(1), dim3(1024), 0, s, a);
+    return hipGetLastError();
 }
 
 // ------------------------------------------------------------- plan upload

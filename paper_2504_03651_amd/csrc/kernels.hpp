@@ -41,15 +41,19 @@ struct AttnArgs {
     float scale_log2;               // sm_scale * log2(e)
     float *out, *part_o, *part_lse;
     int32_t run_log2;               // XCD run length: the caller's minimum, set by the launcher
+    const int32_t *counts;          // device-built plan: its header (word 0 = descriptors);
+                                    // NULL when n_waves is exact
 };
 
 struct PrefillArgs {
     const PrefillDesc *pdesc;
-    int32_t n_pdesc;                // descriptors that get workgroups (chained ones follow)
+    int32_t n_pdesc;                // descriptors that get workgroups (chained ones follow);
+                                    // with `counts`, the capacity of the descriptor region
     int32_t n_logical;              // n_pdesc * num_kv_heads
     int32_t per_xcd;                // logical tiles per XCD slot
     int32_t group;                  // Hq / Hkv (<= 128)
-    const int32_t *klim;
+    const int32_t *seq_lens, *q_start;   // a token's visible keys follow from its row's
+    const int32_t *counts;          // device-built plan: its header (word 1 = descriptors)
     const uint16_t *q;
     int32_t num_q_heads, num_kv_heads;
     const void *k, *v;
@@ -65,12 +69,44 @@ struct PrefillArgs {
 
 struct MergeArgs {
     int64_t n_waves;                // merged rows * ceil(Hq / 4)
+    const int32_t *counts;          // device-built plan: its header (word 2 = merged rows)
     int32_t num_q_heads, head_chunks, heads_per_chunk, group;
     const int32_t *merge_tok, *merge_ptr;
     const int32_t *merge_ent;       // per entry: first slot of its descriptor, nt | i << 10
     const float *part_o, *part_lse;
     float *out;
 };
+
+// The plan of a batch without host mirrors, built on the device into the
+// workspace: no prefix grouping; decode rows cut into pieces of split_keys,
+// prefill rows into tiles of tile_tokens tokens.  Regions have capacities
+// from the host's scalar bounds; the header holds the counts the attention
+// kernels read (DevPlanHeader).
+struct DevPlanArgs {
+    const int32_t *block_tables, *seq_lens, *q_start;
+    const uint8_t *row_kind;
+    int32_t num_rows, num_tokens, max_blocks_per_row, num_blocks, max_seq_len;
+    int32_t split_keys;             // keys per decode piece (multiple of 16)
+    int32_t tile_tokens;            // tokens per prefill tile
+    int32_t slots_per_desc;         // partial slots per decode piece (one token)
+    int32_t prefill_max_keys;       // longest key range the prefill kernel can stage
+    int64_t cap_desc, cap_pdesc, cap_merge_rows, cap_ent, cap_slots;
+    int32_t *row_info;              // [num_rows] scratch: decode pieces | prefill tiles << 16, or -1
+    int32_t *hdr;                   // DevPlanHeader words
+    WorkDesc *desc;
+    PrefillDesc *pdesc;
+    int32_t *merge_tok, *merge_ptr, *merge_ent;
+};
+// words of the header of a device-built plan
+enum DevPlanHeader {
+    kHdrDesc = 0,       // decode descriptors
+    kHdrPdesc = 1,      // prefill descriptors
+    kHdrMergeRows = 2,  // merged tokens
+    kHdrSlots = 3,      // partial slots used
+    kHdrBadRows = 4,    // rows skipped because their metadata is inconsistent
+    kHdrWords = 64
+};
+hipError_t launch_dev_plan(const DevPlanArgs &a, hipStream_t s);
 
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);

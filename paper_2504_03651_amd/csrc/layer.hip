@@ -291,7 +291,8 @@ size_t echo_layer_workspace_bytes(const echo_layer_t *layer, const echo_kv_pool_
 
 int echo_layer_forward(const echo_layer_t *L, const echo_kv_pool_t *pool,
                        const echo_batch_t *batch, void *hidden, void *workspace,
-                       size_t workspace_bytes, void *stream) {
+                       size_t workspace_bytes, void *host_workspace,
+                       size_t host_workspace_bytes, void *stream) {
     echo::clear_error();
     Ws w;
     int rc = plan_ws(L, pool, batch, &w);
@@ -353,7 +354,8 @@ int echo_layer_forward(const echo_layer_t *L, const echo_kv_pool_t *pool,
     if ((rc = echo_kv_append(pool, batch, kn, vn, stream))) return rc;
     mark(4);
     if ((rc = echo_attn_mixed(pool, batch, q, Hq, (float)(1.0 / std::sqrt((double)D)), attn,
-                              base + w.attn_ws, w.attn16 - w.attn_ws, stream)))
+                              base + w.attn_ws, w.attn16 - w.attn_ws, host_workspace,
+                              host_workspace_bytes, stream)))
         return rc;
     mark(5);
     const int64_t n4 = (int64_t)T * Hq * D / 4;

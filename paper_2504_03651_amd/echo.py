@@ -26,7 +26,8 @@ ECHO_E_NOSPACE = -7
 KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
-SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes", "echo_block_copy",
+SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes",
+           "echo_attn_host_workspace_bytes", "echo_block_copy",
            "echo_attn_plan_stats", "echo_attn_plan_pack", "echo_validate", "echo_status_string",
            "echo_last_error",
            "echo_profile", "echo_attn_timing"]
@@ -89,9 +90,11 @@ def lib():
         P, B, vp = ctypes.POINTER(CPool), ctypes.POINTER(CBatch), ctypes.c_void_p
         L.echo_kv_append.argtypes = [P, B, vp, vp, vp]
         L.echo_attn_mixed.argtypes = [P, B, vp, ctypes.c_int32, ctypes.c_float, vp, vp,
-                                      ctypes.c_size_t, vp]
+                                      ctypes.c_size_t, vp, ctypes.c_size_t, vp]
         L.echo_attn_workspace_bytes.argtypes = [P, B, ctypes.c_int32]
         L.echo_attn_workspace_bytes.restype = ctypes.c_size_t
+        L.echo_attn_host_workspace_bytes.argtypes = [P, B, ctypes.c_int32]
+        L.echo_attn_host_workspace_bytes.restype = ctypes.c_size_t
         L.echo_block_copy.argtypes = [P, vp, ctypes.c_int32, vp, vp]
         L.echo_attn_plan_stats.argtypes = [P, B, ctypes.c_int32, ctypes.POINTER(CPlanStats)]
         L.echo_attn_plan_pack.argtypes = [P, B, ctypes.c_int32, ctypes.POINTER(CPlanLayout), vp,
@@ -105,6 +108,11 @@ def lib():
         L.echo_profile.restype = ctypes.c_int
         L.echo_attn_timing.argtypes = [ctypes.POINTER(CAttnTiming)]
         L.echo_attn_timing.restype = ctypes.c_int
+        # the HIP runtime libecho.so links against, for caller-owned pinned memory
+        L.hipHostMalloc.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_size_t, ctypes.c_uint]
+        L.hipHostMalloc.restype = ctypes.c_int
+        L.hipHostFree.argtypes = [ctypes.c_void_p]
+        L.hipHostFree.restype = ctypes.c_int
         for name in ("echo_kv_append", "echo_attn_mixed", "echo_block_copy",
                      "echo_attn_plan_stats", "echo_attn_plan_pack", "echo_validate"):
             getattr(L, name).restype = ctypes.c_int
@@ -220,13 +228,107 @@ def workspace_bytes(pool: KVPool, batch: DeviceBatch, num_q_heads: int) -> int:
     return int(n)
 
 
-def attn_mixed(pool: KVPool, batch: DeviceBatch, q, num_q_heads: int, sm_scale: float, out,
-               workspace, stream=None) -> None:
+def host_workspace_bytes(pool: KVPool, batch: DeviceBatch, num_q_heads: int) -> int:
     cp, cb = pool.c(), batch.c()
+    return int(lib().echo_attn_host_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb),
+                                                    int(num_q_heads)))
+
+
+# hipHostMalloc flags: mapped into the device address space, and coherent
+# (the device reads it uncached, so it sees what the host last wrote)
+_HOST_MAPPED_COHERENT = 0x2 | 0x40000000
+
+
+class HostWorkspace:
+    """Caller-owned pinned host memory for the plans echo_attn_mixed packs
+    and uploads.  A ring of buffers: a buffer is handed out again only after
+    an event recorded behind the call that used it has completed, so the
+    host never rewrites a plan the device has not read yet.  The HIP runtime
+    is the one libecho.so is linked against (resolved through its handle)."""
+
+    def __init__(self, slots: int = 4):
+        self._bufs = [(None, 0)] * slots
+        self._events = [None] * slots
+        self._next = 0
+
+    def acquire(self, nbytes: int):
+        """(pointer, size, slot) of a buffer of at least ``nbytes`` bytes."""
+        i = self._next
+        self._next = (i + 1) % len(self._bufs)
+        ev = self._events[i]
+        if ev is not None:
+            ev.synchronize()
+            self._events[i] = None
+        ptr, size = self._bufs[i]
+        if size < nbytes:
+            L = lib()
+            if ptr:
+                L.hipHostFree(ctypes.c_void_p(ptr))
+                self._bufs[i] = (None, 0)
+            size = max(int(nbytes * 1.5), 1 << 16)
+            p = ctypes.c_void_p()
+            rc = L.hipHostMalloc(ctypes.byref(p), ctypes.c_size_t(size),
+                                 ctypes.c_uint(_HOST_MAPPED_COHERENT))
+            if rc != 0:
+                raise MemoryError(f"hipHostMalloc({size}) failed with HIP error {rc}")
+            ptr = p.value
+            self._bufs[i] = (ptr, size)
+        return ptr, size, i
+
+    def release(self, slot: int, stream) -> None:
+        """Record that the work enqueued on ``stream`` so far reads ``slot``."""
+        import torch
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        self._events[slot] = ev
+
+    def close(self) -> None:
+        for i, (ptr, _) in enumerate(self._bufs):
+            if self._events[i] is not None:
+                self._events[i].synchronize()
+            if ptr:
+                lib().hipHostFree(ctypes.c_void_p(ptr))
+        self._bufs = [(None, 0)] * len(self._bufs)
+        self._events = [None] * len(self._bufs)
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+_default_host_ws = {}
+
+
+def default_host_workspace() -> HostWorkspace:
+    """One host-workspace ring per Python thread."""
+    import threading
+    k = threading.get_ident()
+    if k not in _default_host_ws:
+        _default_host_ws[k] = HostWorkspace()
+    return _default_host_ws[k]
+
+
+def attn_mixed(pool: KVPool, batch: DeviceBatch, q, num_q_heads: int, sm_scale: float, out,
+               workspace, stream=None, host_workspace: HostWorkspace | None = None) -> None:
+    """echo_attn_mixed.  With host mirrors the plan goes through a pinned
+    host buffer of ``host_workspace`` (the calling thread's ring by default);
+    without them the library plans on the device and no host buffer is used."""
+    import torch
+    cp, cb = pool.c(), batch.c()
+    s = torch.cuda.current_stream() if stream is None else stream
+    hptr, hsize, slot = None, 0, None
+    if batch.mirrors and batch.num_rows:
+        hw = host_workspace or default_host_workspace()
+        need = host_workspace_bytes(pool, batch, num_q_heads)
+        hptr, hsize, slot = hw.acquire(need)
     _check(lib().echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), q.data_ptr(),
                                  int(num_q_heads), float(sm_scale), out.data_ptr(),
                                  workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-                                 _stream(stream)), "echo_attn_mixed")
+                                 hptr, hsize, ctypes.c_void_p(s.cuda_stream)), "echo_attn_mixed")
+    if slot is not None:
+        hw.release(slot, s)
 
 
 def block_copy(pool: KVPool, pairs, h_pairs=None, stream=None) -> None:

@@ -41,7 +41,7 @@ def _lib():
         L.echo_layer_workspace_bytes.argtypes = [P, B, ctypes.POINTER(echo.CBatch)]
         L.echo_layer_workspace_bytes.restype = ctypes.c_size_t
         L.echo_layer_forward.argtypes = [P, B, ctypes.POINTER(echo.CBatch), vp, vp,
-                                         ctypes.c_size_t, vp]
+                                         ctypes.c_size_t, vp, ctypes.c_size_t, vp]
         L.echo_layer_forward.restype = ctypes.c_int
         L.echo_layer_timing.argtypes = [ctypes.POINTER(CLayerTiming)]
         L.echo_layer_timing.restype = ctypes.c_int
@@ -71,13 +71,24 @@ class Layer:
             raise echo.EchoError(echo.ECHO_E_INVALID, "echo_layer_workspace_bytes", echo.last_error())
         return int(n)
 
-    def forward(self, pool, batch, hidden, workspace, stream=None) -> None:
-        """hidden: device int16 tensor [T][H] (bf16 bits), overwritten."""
+    def forward(self, pool, batch, hidden, workspace, stream=None, host_workspace=None) -> None:
+        """hidden: device int16 tensor [T][H] (bf16 bits), overwritten.  The
+        attention plan goes through ``host_workspace`` (the calling thread's
+        pinned ring by default) when the batch has host mirrors."""
+        import torch
         cp, cb = pool.c(), batch.c()
+        s = torch.cuda.current_stream() if stream is None else stream
+        hptr, hsize, slot, hw = None, 0, None, None
+        if batch.mirrors and batch.num_rows:
+            hw = host_workspace or echo.default_host_workspace()
+            hptr, hsize, slot = hw.acquire(echo.host_workspace_bytes(pool, batch,
+                                                                     self.lw.num_q_heads))
         echo._check(_lib().echo_layer_forward(
             ctypes.byref(self.c), ctypes.byref(cp), ctypes.byref(cb), hidden.data_ptr(),
             workspace.data_ptr(), workspace.numel() * workspace.element_size(),
-            echo._stream(stream)), "echo_layer_forward")
+            hptr, hsize, ctypes.c_void_p(s.cuda_stream)), "echo_layer_forward")
+        if slot is not None:
+            hw.release(slot, s)
 
 
 def timing() -> dict:

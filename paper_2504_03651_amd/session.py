@@ -38,7 +38,7 @@ class Iteration:
         self.h_cow = np.ascontiguousarray(w.cow_pairs, np.int32).reshape(-1, 2)
         self.cow = torch.from_numpy(self.h_cow).to(device)
         self.workspace = None
-        if mirrors and w.batch.num_rows:
+        if w.batch.num_rows:
             n = echo.workspace_bytes(self.pool, self.batch, Hq)
             self.workspace = torch.empty(n, dtype=torch.uint8, device=device)
 

@@ -157,14 +157,16 @@ def _normal_bf16(seed: int, stream: int, n: int, threads: int | None = None) -> 
 def build(name: str, rows: list, groups: dict, num_q_heads: int, num_kv_heads: int,
           head_dim: int, kv_dtype: str = KV_BF16, num_blocks: int | None = None,
           seed: int = 0, perm_seed: int | None = None, duplicate_prefix: bool = False,
-          pool_factor: float = 1.25) -> Workload:
+          pool_factor: float = 1.25, values: bool = True) -> Workload:
     """Lay ``rows`` onto a paged pool and draw every value.
 
     ``groups`` maps a group id to its shared prefix length in tokens (a
     multiple of 16).  With ``duplicate_prefix`` every row gets private blocks
     holding the same values its group's shared blocks would hold, which is the
     physically duplicated twin of the aliased layout.  ``perm_seed`` reseeds
-    only the placement of blocks in the pool.
+    only the placement of blocks in the pool.  With ``values=False`` only the
+    layout is built (block tables, lengths, copy pairs): q, k_new, v_new,
+    ctx_k and ctx_v are None.
     """
     assert num_q_heads % num_kv_heads == 0
     B = len(rows)
@@ -248,8 +250,9 @@ def build(name: str, rows: list, groups: dict, num_q_heads: int, num_kv_heads: i
     coff = np.zeros(len(cfill) + 1, dtype=np.int64)
     coff[1:] = np.cumsum(cfill)
     ntok = int(coff[-1])
-    ck = _normal_bf16(seed, 2, ntok * Hkv * D).reshape(ntok, Hkv, D)
-    cv = _normal_bf16(seed, 3, ntok * Hkv * D).reshape(ntok, Hkv, D)
+    if values:
+        ck = _normal_bf16(seed, 2, ntok * Hkv * D).reshape(ntok, Hkv, D)
+        cv = _normal_bf16(seed, 3, ntok * Hkv * D).reshape(ntok, Hkv, D)
 
     # one pseudo-row per physical block holding context, in content order
     holders = [[] for _ in range(len(cfill))]
@@ -269,16 +272,20 @@ def build(name: str, rows: list, groups: dict, num_q_heads: int, num_kv_heads: i
     ctx_qs = np.zeros(nctx + 1, dtype=np.int32)
     ctx_qs[1:] = np.cumsum(ctx_len)
     ctx = Batch(ctx_bt, ctx_len.copy(), ctx_qs, np.full(nctx, PREFILL, dtype=np.uint8))
-    if nctx == int((cfill > 0).sum()):
+    if not values:
+        ctx_k = ctx_v = None
+    elif nctx == int((cfill > 0).sum()):
         ctx_k, ctx_v = ck, cv
     else:
         idx = np.concatenate([np.arange(coff[c], coff[c] + cfill[c]) for c in ctx_cont])
         ctx_k, ctx_v = ck[idx], cv[idx]
 
     T = int(q_start[-1])
-    k_new = _normal_bf16(seed, 4, T * Hkv * D).reshape(T, Hkv, D)
-    v_new = _normal_bf16(seed, 5, T * Hkv * D).reshape(T, Hkv, D)
-    q = _normal_bf16(seed, 6, T * Hq * D).reshape(T, Hq, D)
+    k_new = v_new = q = None
+    if values:
+        k_new = _normal_bf16(seed, 4, T * Hkv * D).reshape(T, Hkv, D)
+        v_new = _normal_bf16(seed, 5, T * Hkv * D).reshape(T, Hkv, D)
+        q = _normal_bf16(seed, 6, T * Hq * D).reshape(T, Hq, D)
 
     # one copy-on-write fork per prefix group into a block nobody reads
     free = perm[n_phys:]

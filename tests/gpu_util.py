@@ -2,7 +2,9 @@
 from __future__ import annotations
 
 import copy
+import os
 import sys
+from concurrent.futures import ThreadPoolExecutor
 
 import numpy as np
 
@@ -72,3 +74,64 @@ def sample_queries(w, n, seed=0):
             for h in (0, Hq - 1):
                 picks.add(t * Hq + h)
     return np.array(sorted(picks), dtype=np.int32)
+
+
+def cpu_share() -> int:
+    """Host threads this process may use: its CPU affinity, capped by the
+    cgroup's CPU quota when one is set."""
+    n = len(os.sched_getaffinity(0))
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            quota, period = f.read().split()[:2]
+        if quota != "max":
+            n = min(n, max(1, int(quota) // int(period)))
+    except (OSError, ValueError):
+        pass
+    return max(1, n)
+
+
+def oracle_pool(c, threads=None):
+    """``oracle.prepare(c)`` with the context append spread over host threads.
+    The context batch has one pseudo-row per physical block, so its rows write
+    disjoint blocks and any split of them gives the same pool."""
+    ctx = c.ctx
+    B = ctx.num_rows
+    ids = ctx.block_tables[:, 0]
+    assert len(np.unique(ids)) == B, "context rows must write disjoint blocks"
+    pool = oracle.Pool(c.num_blocks, c.num_kv_heads, c.head_dim, c.kv_dtype != W.KV_BF16)
+    threads = threads or cpu_share()
+    cuts = np.linspace(0, B, min(threads, max(B, 1)) + 1).astype(np.int64)
+    qs = ctx.q_start
+
+    def part(i):
+        r0, r1 = int(cuts[i]), int(cuts[i + 1])
+        if r1 <= r0:
+            return
+        sub = W.Batch(ctx.block_tables[r0:r1], ctx.seq_lens[r0:r1],
+                      (qs[r0:r1 + 1] - qs[r0]).astype(np.int32), ctx.row_kind[r0:r1])
+        t0, t1 = int(qs[r0]), int(qs[r1])
+        oracle.kv_append(pool, sub, c.ctx_k[t0:t1], c.ctx_v[t0:t1])
+
+    with ThreadPoolExecutor(len(cuts) - 1) as ex:
+        list(ex.map(part, range(len(cuts) - 1)))
+    return pool
+
+
+def tile_queries(w, tiles_per_chunk=3):
+    """Query indices t*Hq + h of every decode token and of whole prefill
+    tiles (all query heads of 256 / G consecutive tokens, the tiles of the
+    prefill kernel): the first, middle and last tile of every chunk."""
+    Hq, Hkv = w.num_q_heads, w.num_kv_heads
+    bt = max(1, 256 // (Hq // Hkv))
+    qs, kind = w.batch.q_start, w.batch.row_kind
+    toks = []
+    for r in range(w.batch.num_rows):
+        t0, t1 = int(qs[r]), int(qs[r + 1])
+        if kind[r] == W.DECODE:
+            toks.append(np.arange(t0, t1))
+            continue
+        n = (t1 - t0 + bt - 1) // bt
+        for k in sorted({0, n // 2, n - 1} if tiles_per_chunk >= 3 else {0, n - 1}):
+            toks.append(np.arange(t0 + k * bt, min(t1, t0 + (k + 1) * bt)))
+    toks = np.unique(np.concatenate(toks))
+    return (toks[:, None] * Hq + np.arange(Hq)[None, :]).ravel().astype(np.int32)

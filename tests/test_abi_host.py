@@ -112,12 +112,63 @@ def test_partial_mirrors_rejected():
     assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
 
 
-def test_attention_without_mirrors_is_rejected_before_any_work():
+def test_attention_without_mirrors_sizes_from_scalars():
+    # without host mirrors the plan is built on the device: the workspace is a
+    # bound from the scalar fields and no host workspace is needed
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    L = echo.lib()
+    with_mirrors = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    assert L.echo_attn_host_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4) > 0
+    cb.h_block_tables = cb.h_seq_lens = cb.h_q_start = cb.h_row_kind = None
+    n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    assert n > 0 and n % 256 == 0 and with_mirrors > 0
+    assert L.echo_attn_host_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4) == 0
+    # the bound grows with the scalars it is taken from
+    mbr, msl = cb.max_blocks_per_row, cb.max_seq_len
+    cb.max_blocks_per_row, cb.max_seq_len = 64, 1000   # sizing only: no table is read
+    assert L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4) > n
+    cb.max_blocks_per_row, cb.max_seq_len = mbr, msl
+    cb.num_rows, cb.num_tokens = cb.num_rows * 2, cb.num_tokens * 2
+    assert L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4) > n
+
+
+def _attn(L, cp, cb, hq, ws, ws_bytes, hws, hws_bytes):
+    fake = ctypes.c_void_p(256)   # q / out: never dereferenced, a check fails first
+    return L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, hq, 0.125, fake,
+                             ws, ws_bytes, hws, hws_bytes, None)
+
+
+def test_attention_workspace_errors_with_mirrors():
+    w = W.config1()
+    cp, cb, keep = _structs(w)
+    L = echo.lib()
+    n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    hn = L.echo_attn_host_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    host = np.zeros(hn + 64, np.uint8)    # pageable memory: refused as host workspace
+    hp = ctypes.c_void_p(host.ctypes.data + (-host.ctypes.data) % 16)
+    dev = ctypes.c_void_p(1 << 20)        # a 256-byte aligned stand-in, never touched
+    for args, what in [((None, n, hp, hn), "workspace of"),
+                       ((dev, n - 4, hp, hn), "workspace of"),
+                       ((ctypes.c_void_p((1 << 20) + 128), n, hp, hn), "256-byte aligned"),
+                       ((dev, n, None, hn), "host workspace of"),
+                       ((dev, n, hp, hn - 4), "host workspace of"),
+                       ((dev, n, ctypes.c_void_p(hp.value + 4), hn), "16-byte aligned"),
+                       ((dev, n, hp, hn), "not pinned")]:
+        rc = _attn(L, cp, cb, 4, *args)
+        assert rc == echo.ECHO_E_WORKSPACE and what in echo.last_error(), (what, echo.last_error())
+
+
+def test_attention_workspace_errors_without_mirrors():
     w = W.config1()
     cp, cb, keep = _structs(w)
     cb.h_block_tables = cb.h_seq_lens = cb.h_q_start = cb.h_row_kind = None
-    n = echo.lib().echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
-    assert n == 0 and "host mirrors" in echo.last_error()
+    L = echo.lib()
+    n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 4)
+    for ws, nb, what in [(None, n, "workspace of"), (ctypes.c_void_p(1 << 20), n - 256, "workspace of"),
+                         (ctypes.c_void_p((1 << 20) + 64), n, "256-byte aligned")]:
+        rc = _attn(L, cp, cb, 4, ws, nb, None, 0)
+        assert rc == echo.ECHO_E_WORKSPACE and what in echo.last_error(), echo.last_error()
 
 
 @pytest.mark.parametrize("scale", [0.0, -0.125, float("nan"), float("inf")])
@@ -127,7 +178,7 @@ def test_attention_rejects_non_positive_scale(scale):
     cp, cb, keep = _structs(w)
     fake = ctypes.c_void_p(256)   # never dereferenced: validation fails first
     rc = echo.lib().echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 4, scale, fake,
-                                    None, 0, None)
+                                    None, 0, None, 0, None)
     assert rc == echo.ECHO_E_INVALID and "sm_scale" in echo.last_error()
 
 
@@ -142,7 +193,8 @@ def test_prefill_row_beyond_the_staging_limit():
     n = L.echo_attn_workspace_bytes(ctypes.byref(cp), ctypes.byref(cb), 8)
     assert n > 0
     fake = ctypes.c_void_p(256)   # never dereferenced: the check comes first
-    rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 8, 0.088, fake, fake, n, None)
+    rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), fake, 8, 0.088, fake, fake, n,
+                           None, 0, None)
     assert rc == echo.ECHO_E_UNSUPPORTED
     assert "16373 blocks exceeds the 16372-block limit" in echo.last_error()
 

@@ -2,9 +2,9 @@
 
 Each thread owns a pool, a workspace and a stream (default priority) and
 repeats its iteration; the library is entered from all threads at once (the
-binding releases the interpreter lock during calls), so plan buffers, the
-shared pinned staging ring and the per-thread timing state are exercised
-under contention.  Every thread's final pool and outputs must match the
+binding releases the interpreter lock during calls), so the per-thread plan
+buffers, each thread's pinned host-workspace ring and the per-thread timing
+state are exercised under contention.  Every thread's final pool and outputs must match the
 oracle, as in the single-stream parity tests.
 """
 import threading

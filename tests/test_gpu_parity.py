@@ -3,14 +3,18 @@
 Append and block copy must match bit for bit (whole pools for small cases,
 every block the batch touches for full-size ones).  Attention outputs must
 stay within ATOL (max abs error) of the oracle: all outputs for small and
-fuzzed cases, sampled outputs at the five serving-shaped configurations.
+fuzzed cases and for the full-size decode-only and mixed configurations; for
+the long-context and e4m3 configurations every decode output and whole
+prefill tiles (first, middle and last of every chunk).  Both planning modes
+run: with host mirrors (host plan, prefix groups) and without (device plan).
 """
 import numpy as np
 import pytest
 
 import oracle
 from paper_2504_03651_amd import workload as W
-from tests.gpu_util import ATOL, attn_error, compact, same_pool, sample_queries, say
+from tests.gpu_util import (ATOL, attn_error, compact, cpu_share, oracle_pool, same_pool,
+                            sample_queries, say, tile_queries)
 
 pytestmark = pytest.mark.gpu
 
@@ -187,6 +191,8 @@ def test_empty_batch(torch_cuda):
     out = torch_cuda.zeros(1, dtype=torch_cuda.float32, device="cuda")
     ws = torch_cuda.empty(256, dtype=torch_cuda.uint8, device="cuda")
     echo.attn_mixed(pool, b, z, 4, 0.125, out, ws)
+    b.mirrors = False
+    echo.attn_mixed(pool, b, z, 4, 0.125, out, ws)
     torch_cuda.cuda.synchronize()
 
 
@@ -254,20 +260,166 @@ def test_prefill_at_the_staging_limit(torch_cuda):
 
 @pytest.mark.parametrize("cfg", [2, 3, 4, 5])
 def test_full_size_config(torch_cuda, cfg):
+    # the launch configuration bench.py times: host mirrors, host plan
     w = W.config(cfg)
+    th = cpu_share()
     say(f"[case] config{cfg} full size: rows={w.batch.num_rows} T={w.batch.num_tokens} "
-        f"NB={w.num_blocks} kv={w.kv_dtype}")
+        f"NB={w.num_blocks} kv={w.kv_dtype} (oracle on {th} threads)")
     it = _run(w, torch_cuda)
+    out = it.out.cpu().numpy().reshape(-1, w.head_dim)
+    assert not np.isnan(out).any()
     c, ids = compact(w)
-    pool = oracle.prepare(c)
+    pool = oracle_pool(c, th)
     oracle.block_copy(pool, c.cow_pairs)
     oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
     say("       comparing touched blocks bit for bit")
     same_pool(it.pool_host(ids), pool)
-    sel = sample_queries(w, 768, seed=cfg)
-    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, sel=sel)
-    got = it.out.cpu().numpy().reshape(-1, w.head_dim)[sel]
-    assert not np.isnan(it.out.cpu().numpy()).any()
+    # every output where the oracle takes seconds; else every decode output
+    # and whole prefill tiles
+    sel = None if cfg in (2, 3) else tile_queries(w)
+    what = "all" if sel is None else f"{len(sel)} of {out.shape[0]}"
+    say(f"       oracle attention over {what} query vectors")
+    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, sel=sel, threads=th)
+    got = out if sel is None else out[sel]
     err, nerr = attn_error(got, ref)
-    say(f"       {len(sel)} sampled outputs: max abs err {err:.3e}  normalised {nerr:.3e}")
+    say(f"       {what} outputs: max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
+
+
+# --------------------------------------------------------- non-power-of-two groups
+
+GQA = [(g, hkv, d, kv) for g, hkv, d in ((3, 2, 128), (6, 2, 64), (12, 1, 128), (24, 2, 128))
+       for kv in (W.KV_BF16, W.KV_FP8)]
+
+
+@pytest.mark.parametrize("case", GQA, ids=[f"g{c[0]}-d{c[2]}-{c[3]}" for c in GQA])
+def test_gqa_groups_not_powers_of_two(torch_cuda, case):
+    # query heads per KV head of 3, 6, 12 and 24: partial lanes of a decode
+    # wave's 16 query vectors, two head chunks (24), prefill tiles of 85, 42,
+    # 21 and 10 tokens
+    g, hkv, d, kv = case
+    w = W.random_case(210 + g, num_rows=9, num_q_heads=g * hkv, num_kv_heads=hkv, head_dim=d,
+                      kv_dtype=kv, max_ctx=2000, max_q=150, n_groups=2)
+    _check_small(w, torch_cuda, f"gqa{g}-{kv}")
+
+
+# ------------------------------------------------------ plan built on the device
+
+NOMIRROR = [
+    ("cfg1", lambda: W.config1()),
+    ("random-301", lambda: W.random_case(301, num_rows=8, num_q_heads=8, num_kv_heads=2,
+                                         head_dim=128, max_ctx=3000, max_q=200, n_groups=2)),
+    ("random-302-e4m3", lambda: W.random_case(302, num_rows=7, num_q_heads=32, num_kv_heads=8,
+                                              head_dim=128, kv_dtype=W.KV_FP8, max_ctx=2500,
+                                              max_q=120, n_groups=2)),
+    ("random-303-gqa6", lambda: W.random_case(303, num_rows=9, num_q_heads=12, num_kv_heads=2,
+                                              head_dim=64, max_ctx=1500, max_q=90, n_groups=3)),
+    ("random-304-gqa24", lambda: W.random_case(304, num_rows=6, num_q_heads=48, num_kv_heads=2,
+                                               head_dim=128, max_ctx=1200, max_q=60)),
+    ("many-rows", lambda: W.random_case(305, num_rows=1500, num_q_heads=4, num_kv_heads=2,
+                                        head_dim=64, max_ctx=90, max_q=20, n_groups=3)),
+]
+
+
+@pytest.mark.parametrize("make", [m for _, m in NOMIRROR], ids=[n for n, _ in NOMIRROR])
+def test_attention_without_mirrors(torch_cuda, make):
+    # the same iteration, planned on the device (no prefix grouping): outputs
+    # within ATOL of the oracle and of the host-planned path
+    w = make()
+    say(f"[case] no mirrors {w.name}: rows={w.batch.num_rows} T={w.batch.num_tokens} "
+        f"Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} kv={w.kv_dtype}")
+    it = _run(w, torch_cuda, mirrors=False)
+    pool, ref = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    got = it.out.cpu().numpy().reshape(ref.shape)
+    err, nerr = attn_error(got, ref)
+    say(f"       max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
+    hdr = it.workspace[:64 * 4].view(torch_cuda.int32).cpu().numpy()
+    assert hdr[4] == 0, "no row may be skipped"
+    host = _run(w, torch_cuda).out.cpu().numpy().reshape(ref.shape)
+    assert np.abs(host - got).max() <= ATOL
+
+
+def test_attention_without_mirrors_full_size_config3(torch_cuda):
+    w = W.config(3)
+    th = cpu_share()
+    say(f"[case] no mirrors config3 full size (oracle on {th} threads)")
+    it = _run(w, torch_cuda, mirrors=False)
+    out = it.out.cpu().numpy().reshape(-1, w.head_dim)
+    c, ids = compact(w)
+    pool = oracle_pool(c, th)
+    oracle.block_copy(pool, c.cow_pairs)
+    oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
+    same_pool(it.pool_host(ids), pool)
+    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, threads=th)
+    err, nerr = attn_error(out, ref)
+    say(f"       all outputs: max abs err {err:.3e}  normalised {nerr:.3e}")
+    assert err <= ATOL
+
+
+def test_attention_without_mirrors_skips_inconsistent_rows(torch_cuda):
+    # a decode row whose block table names a block outside the pool, and a
+    # prefill row with more keys than its block table holds: both are skipped
+    # by the device planner (their outputs stay as they were), the others match
+    w = W.random_case(306, num_rows=8, num_q_heads=8, num_kv_heads=2, head_dim=128,
+                      max_ctx=800, max_q=50, n_groups=2)
+    say("[case] no mirrors, inconsistent rows")
+    from paper_2504_03651_amd.session import Iteration
+    it = Iteration(w, mirrors=False)
+    it.copy()
+    it.append()
+    kind = w.batch.row_kind
+    rd = int(np.flatnonzero(kind == W.DECODE)[0])
+    rp = int(np.flatnonzero(kind == W.PREFILL)[0])
+    it.batch.bt[rd, 0] = w.num_blocks + 7
+    it.batch.sl[rp] = it.batch.max_seq_len + 1
+    it.out.fill_(7.0)
+    it.attend()
+    torch_cuda.cuda.synchronize()
+    hdr = it.workspace[:64 * 4].view(torch_cuda.int32).cpu().numpy()
+    assert hdr[4] == 2
+    pool, ref = oracle.run_iteration(w)
+    got = it.out.cpu().numpy().reshape(w.batch.num_tokens, w.num_q_heads, w.head_dim)
+    ref = ref.reshape(got.shape)
+    qs = w.batch.q_start
+    skipped = np.zeros(w.batch.num_tokens, bool)
+    for r in (rd, rp):
+        skipped[qs[r]:qs[r + 1]] = True
+    assert (got[skipped] == 7.0).all()
+    assert np.abs(got[~skipped] - ref[~skipped]).max() <= ATOL
+
+
+def test_host_workspace_must_be_pinned(torch_cuda):
+    import ctypes
+    from paper_2504_03651_amd import echo
+    from paper_2504_03651_amd.session import Iteration
+    w = W.config1()
+    say("[case] host workspace: pageable memory refused, pinned accepted")
+    it = Iteration(w)
+    it.copy()
+    it.append()
+    cp, cb = it.pool.c(), it.batch.c()
+    n = echo.host_workspace_bytes(it.pool, it.batch, w.num_q_heads)
+    pageable = np.zeros(n + 16, np.uint8)
+    L = echo.lib()
+    s = ctypes.c_void_p(torch_cuda.cuda.current_stream().cuda_stream)
+    ws = it.workspace
+    rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), it.q.data_ptr(), w.num_q_heads,
+                           w.sm_scale, it.out.data_ptr(), ws.data_ptr(), ws.numel(),
+                           ctypes.c_void_p(pageable.ctypes.data), n, s)
+    assert rc == echo.ECHO_E_WORKSPACE and "pinned" in echo.last_error()
+    hw = echo.HostWorkspace(slots=1)
+    try:
+        ptr, size, slot = hw.acquire(n)
+        rc = L.echo_attn_mixed(ctypes.byref(cp), ctypes.byref(cb), it.q.data_ptr(),
+                               w.num_q_heads, w.sm_scale, it.out.data_ptr(), ws.data_ptr(),
+                               ws.numel(), ctypes.c_void_p(ptr), size, s)
+        assert rc == echo.ECHO_OK, echo.last_error()
+        hw.release(slot, torch_cuda.cuda.current_stream())
+        torch_cuda.cuda.synchronize()
+    finally:
+        hw.close()
+    pool, ref = oracle.run_iteration(w)
+    err, _ = attn_error(it.out.cpu().numpy().reshape(ref.shape), ref)
     assert err <= ATOL

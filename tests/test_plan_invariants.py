@@ -31,21 +31,31 @@ def _one_round_case(kv=W.KV_BF16):
 
 
 def _cases():
-    yield W.config1()
-    yield W.config1(share_with_prefill=True)
+    """(id, builder) pairs; workloads are built inside the test (layouts only
+    for the full-size configurations, whose values the plan never reads)."""
+    yield "cfg1", lambda: W.config1()
+    yield "cfg1-share-prefill", lambda: W.config1(share_with_prefill=True)
     for seed in (201, 202, 203):
-        yield W.random_case(seed, num_rows=9, num_q_heads=8, num_kv_heads=2, head_dim=128,
-                            max_ctx=2500, max_q=120, n_groups=3)
-    yield W.random_case(204, num_rows=7, num_q_heads=32, num_kv_heads=1, head_dim=64,
-                        max_ctx=3000, max_q=60, n_groups=2)
+        yield f"random-{seed}", lambda seed=seed: W.random_case(
+            seed, num_rows=9, num_q_heads=8, num_kv_heads=2, head_dim=128, max_ctx=2500,
+            max_q=120, n_groups=3)
+    yield "random-204", lambda: W.random_case(204, num_rows=7, num_q_heads=32, num_kv_heads=1,
+                                              head_dim=64, max_ctx=3000, max_q=60, n_groups=2)
     for hq, hkv in ((32, 1), (8, 2), (4, 4)):
         rows = [W.RowSpec(W.PREFILL, 3000, 40), W.RowSpec(W.DECODE, 700, 1),
                 W.RowSpec(W.PREFILL, 1500, 300), W.RowSpec(W.PREFILL, 64, 17)]
-        yield W.build(f"split-{hq}-{hkv}", rows, {}, hq, hkv, 128, seed=118)
-    yield W.config(3)
-    yield _one_round_case()
-    yield W.random_case(205, num_rows=600, num_q_heads=4, num_kv_heads=2, head_dim=64,
-                        max_ctx=100, max_q=30, n_groups=3)
+        yield f"split-{hq}-{hkv}", lambda hq=hq, hkv=hkv, rows=rows: W.build(
+            f"split-{hq}-{hkv}", rows, {}, hq, hkv, 128, seed=118)
+    # query heads per KV head that are not powers of two (3, 6, 12, 24)
+    for g, hkv, d in ((3, 2, 128), (6, 2, 64), (12, 1, 128), (24, 2, 128)):
+        yield f"gqa{g}", lambda g=g, hkv=hkv, d=d: W.random_case(
+            210 + g, num_rows=9, num_q_heads=g * hkv, num_kv_heads=hkv, head_dim=d,
+            max_ctx=2000, max_q=150, n_groups=2)
+    for cfg in (2, 3, 4, 5):
+        yield f"cfg{cfg}", lambda cfg=cfg: W.config(cfg, values=False)
+    yield "one-round", lambda: _one_round_case()
+    yield "random-205", lambda: W.random_case(205, num_rows=600, num_q_heads=4, num_kv_heads=2,
+                                              head_dim=64, max_ctx=100, max_q=30, n_groups=3)
 
 
 CASES = list(_cases())
@@ -57,8 +67,9 @@ def _decode(w):
     return lay, words
 
 
-@pytest.mark.parametrize("w", CASES, ids=[c.name for c in CASES])
-def test_plan_invariants(w):
+@pytest.mark.parametrize("make", [m for _, m in CASES], ids=[n for n, _ in CASES])
+def test_plan_invariants(make):
+    w = make()
     lay, words = _decode(w)
     b = w.batch
     B, T = b.num_rows, b.num_tokens
@@ -222,7 +233,7 @@ def test_one_round_prefill_balanced():
     # the mixed batch's 2,048-token chunk on 1,024 cached tokens: 32 tiles of
     # 17..48 64-key tiles per KV head, 256 workgroups; the longest workgroup
     # walks 34 (mean 32.5; a tile only 1 over the target of 33 keeps its keys)
-    work, orig, chains = _prefill_work(W.config(3))
+    work, orig, chains = _prefill_work(W.config(3, values=False))
     assert max(orig) == 48 and chains == 14
     assert max(work) == 34 and sum(work) == sum(orig)
     # two chunks of unequal lengths (tiles of 1..16 and 33..40, mean 17.8): a
@@ -231,7 +242,7 @@ def test_one_round_prefill_balanced():
     work, orig, chains = _prefill_work(_one_round_case())
     assert max(orig) == 40 and max(work) == 19 and sum(work) == sum(orig)
     # more than one round of workgroups: no chains
-    assert _prefill_work(W.config(5))[2] == 0
+    assert _prefill_work(W.config(5, values=False))[2] == 0
 
 
 def test_plan_pack_buffer_too_small():
@@ -251,18 +262,18 @@ def test_plan_pack_buffer_too_small():
 def test_small_decode_batches_split_finer():
     # a late prefill chunk next to a few long decode rows: 48-block pieces
     # would give 24 descriptors; the planner shrinks them (not below 8 blocks)
-    w = W.config(6)
+    w = W.config(6, values=False)
     lay, words = _decode(w)
     d = words[lay["off_desc"]:lay["off_desc"] + 8 * lay["n_desc"]].reshape(-1, 8)
     blocks = (d[:, 4] - d[:, 3] + 15) // 16
     assert len(d) > 24 and blocks.max() <= 8
     # a large batch keeps the long pieces
-    w2 = W.config(2)
+    w2 = W.config(2, values=False)
     lay2, words2 = _decode(w2)
     d2 = words2[lay2["off_desc"]:lay2["off_desc"] + 8 * lay2["n_desc"]].reshape(-1, 8)
     assert ((d2[:, 4] - d2[:, 3] + 15) // 16).max() == 48
     # e4m3 pieces hold as many bytes: twice the blocks
-    w5 = W.config(5)
+    w5 = W.config(5, values=False)
     lay5, words5 = _decode(w5)
     d5 = words5[lay5["off_desc"]:lay5["off_desc"] + 8 * lay5["n_desc"]].reshape(-1, 8)
     assert ((d5[:, 4] - d5[:, 3] + 15) // 16).max() == 96
