@@ -169,6 +169,22 @@ size_t echo_attn_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t 
 size_t echo_attn_host_workspace_bytes(const echo_kv_pool_t *pool, const echo_batch_t *batch,
                                       int32_t num_q_heads);
 
+/* Mixed attention that allocates nothing and takes no workspace, for
+ * callers that cannot allocate device memory: code under HIP graph capture,
+ * tight serving loops, harnesses that forbid allocation.  Same arguments,
+ * results and checks as echo_attn_mixed, always with the plan built on the
+ * device (host mirrors, when given, are used for validation only).  The plan
+ * and the partial results live in a static device array of the library
+ * (32 MiB, held by each GPU the library runs on until the process ends);
+ * a batch whose device-built plan needs more returns ECHO_E_WORKSPACE before
+ * anything is enqueued.  Every call on a GPU uses that GPU's one array and
+ * leaves its contents behind; every word a call reads is written earlier in
+ * the same call, so nothing needs clearing, but calls that overlap on one
+ * GPU (other streams, other host threads) race and must be serialised by
+ * the caller. */
+int echo_attn_mixed_static(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
+                           int32_t num_q_heads, float sm_scale, float *out, void *stream);
+
 /* Block copy (copy-on-write of blocks that prefix-sharing rows alias; the
  * paper's automatic prefix caching, Section 6, implies it).  For each pair
  * (src, dst) of pairs (device int32 [n][2]) copies K, V and, for e4m3 pools,

@@ -459,7 +459,7 @@ int check_attn_args(const echo_kv_pool_t *pool, const echo_batch_t *batch, int32
 // attention kernels reading their counts from the plan's header.
 int attn_device_planned(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
                         int32_t num_q_heads, float sm_scale, float *out, void *workspace,
-                        size_t workspace_bytes, hipStream_t s) {
+                        size_t workspace_bytes, hipStream_t s, bool allow_profile = true) {
     DevLayout L;
     int rc = dev_layout(pool, batch, num_q_heads, L);
     if (rc) return rc;
@@ -469,8 +469,10 @@ int attn_device_planned(const echo_kv_pool_t *pool, const echo_batch_t *batch, c
     if (((uintptr_t)workspace & 255u) != 0)
         return fail(ECHO_E_WORKSPACE, "workspace must be 256-byte aligned");
     hipEvent_t *ev = nullptr;
-    rc = profile_events(&ev);
-    if (rc) return rc;
+    if (allow_profile) {
+        rc = profile_events(&ev);
+        if (rc) return rc;
+    }
     g_prof.valid = false;
     int32_t *w = (int32_t *)workspace;
     DevPlanArgs d;
@@ -822,6 +824,30 @@ int echo_attn_mixed(const echo_kv_pool_t *pool, const echo_batch_t *batch, const
     a.run_log2 = run_log2_for(plan.sibling_waves);
     a.pf_max_blocks = pf_blocks;
     return launch_attention(pool, batch, q, num_q_heads, sm_scale, out, a, s, ev);
+}
+
+int echo_attn_mixed_static(const echo_kv_pool_t *pool, const echo_batch_t *batch, const void *q,
+                           int32_t num_q_heads, float sm_scale, float *out, void *stream) {
+    g_error.clear();
+    int rc = check_attn_args(pool, batch, num_q_heads);
+    if (rc) return rc;
+    if (batch->num_rows == 0) return ECHO_OK;
+    if (!q || !out) return fail(ECHO_E_INVALID, "q / out is NULL");
+    if (!(sm_scale > 0.f) || !std::isfinite(sm_scale))
+        return fail(ECHO_E_INVALID, "sm_scale must be positive and finite");
+    DevLayout L;
+    rc = dev_layout(pool, batch, num_q_heads, L);
+    if (rc) return rc;
+    const size_t need = (size_t)L.total_words * 4;
+    if (need > kScratchBytes)
+        return fail(ECHO_E_WORKSPACE,
+                    "batch needs %zu bytes of scratch; the static scratch holds %zu (use "
+                    "echo_attn_mixed with a workspace)", need, kScratchBytes);
+    void *ptr = nullptr;
+    hipError_t e = scratch_region(&ptr);
+    if (e != hipSuccess) return hip_fail(e, "hipGetSymbolAddress (static scratch)");
+    return attn_device_planned(pool, batch, q, num_q_heads, sm_scale, out, ptr, kScratchBytes,
+                               (hipStream_t)stream, false);
 }
 
 }  // extern "C"

@@ -1442,6 +1442,33 @@ hipError_t launch_dev_plan(const DevPlanArgs &a, hipStream_t s) {
     return hipGetLastError();
 }
 
+// ----------------------------------------------------------- static scratch
+//
+// Device memory of echo_attn_mixed_static: the plan and partial results of
+// a device-planned call live here instead of in a caller's workspace.  Each
+// GPU the library runs on holds its own copy for the life of the process.
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+// Address of this device's copy of `scratch`, looked up once per device
+// with that device current (in host code the array's name is not a device
+// address).
+hipError_t scratch_region(void **ptr) {
+    static std::atomic<void *> addr[64];
+    int dev = 0;
+    hipError_t e = hipGetDevice(&dev);
+    if (e != hipSuccess) return e;
+    if (dev < 0 || dev >= 64) return hipErrorInvalidDevice;
+    void *p = addr[dev].load(std::memory_order_acquire);
+    if (!p) {
+        e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+        if (e != hipSuccess) return e;
+        if (!p) return hipErrorInvalidSymbol;
+        addr[dev].store(p, std::memory_order_release);
+    }
+    *ptr = p;
+    return hipSuccess;
+}
+
 // ------------------------------------------------------------- plan upload
 //
 // Copies the packed plan from pinned, coherent host memory into the

@@ -108,6 +108,11 @@ enum DevPlanHeader {
 };
 hipError_t launch_dev_plan(const DevPlanArgs &a, hipStream_t s);
 
+// Static device scratch of echo_attn_mixed_static (a file-scope __device__
+// array in kernels.hip): its size, and this device's address of it.
+constexpr size_t kScratchBytes = (size_t)32 << 20;
+hipError_t scratch_region(void **ptr);
+
 hipError_t launch_append(const AppendArgs &a, int head_dim, bool fp8, hipStream_t s);
 hipError_t launch_block_copy(const BlockCopyArgs &a, hipStream_t s);
 // Copies `words` 32-bit words from device-visible pinned host memory to dst.

@@ -27,7 +27,7 @@ KV_BF16 = 0
 KV_FP8_E4M3 = 1
 
 SYMBOLS = ["echo_kv_append", "echo_attn_mixed", "echo_attn_workspace_bytes",
-           "echo_attn_host_workspace_bytes", "echo_block_copy",
+           "echo_attn_host_workspace_bytes", "echo_attn_mixed_static", "echo_block_copy",
            "echo_attn_plan_stats", "echo_attn_plan_pack", "echo_validate", "echo_status_string",
            "echo_last_error",
            "echo_profile", "echo_attn_timing"]
@@ -93,6 +93,8 @@ def lib():
                                       ctypes.c_size_t, vp, ctypes.c_size_t, vp]
         L.echo_attn_workspace_bytes.argtypes = [P, B, ctypes.c_int32]
         L.echo_attn_workspace_bytes.restype = ctypes.c_size_t
+        L.echo_attn_mixed_static.argtypes = [P, B, vp, ctypes.c_int32, ctypes.c_float, vp, vp]
+        L.echo_attn_mixed_static.restype = ctypes.c_int
         L.echo_attn_host_workspace_bytes.argtypes = [P, B, ctypes.c_int32]
         L.echo_attn_host_workspace_bytes.restype = ctypes.c_size_t
         L.echo_block_copy.argtypes = [P, vp, ctypes.c_int32, vp, vp]
@@ -329,6 +331,15 @@ def attn_mixed(pool: KVPool, batch: DeviceBatch, q, num_q_heads: int, sm_scale: 
                                  hptr, hsize, ctypes.c_void_p(s.cuda_stream)), "echo_attn_mixed")
     if slot is not None:
         hw.release(slot, s)
+
+
+def attn_mixed_static(pool: KVPool, batch: DeviceBatch, q, num_q_heads: int, sm_scale: float,
+                      out, stream=None) -> None:
+    """echo_attn_mixed_static: no workspace, the library's static scratch."""
+    cp, cb = pool.c(), batch.c()
+    _check(lib().echo_attn_mixed_static(ctypes.byref(cp), ctypes.byref(cb), q.data_ptr(),
+                                        int(num_q_heads), float(sm_scale), out.data_ptr(),
+                                        _stream(stream)), "echo_attn_mixed_static")
 
 
 def block_copy(pool: KVPool, pairs, h_pairs=None, stream=None) -> None:

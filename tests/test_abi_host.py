@@ -249,3 +249,16 @@ def test_plan_shares_prefix_blocks_in_config1():
     dup = W.config1(duplicate_prefix=True)
     cp, cb, keep = _structs(dup)
     assert echo.plan_stats(cp, cb, dup.num_q_heads)["shared_segments"] == 0
+
+
+def test_static_entry_refuses_batches_beyond_its_scratch():
+    # the e4m3 mixed configuration's device-built plan needs about 100 MB of
+    # partial results, more than the 32 MiB static scratch: refused before
+    # any GPU work, with the sizes in the message
+    w = W.config(5, values=False)
+    cp, cb, keep = _structs(w)
+    fake = ctypes.c_void_p(256)
+    rc = echo.lib().echo_attn_mixed_static(ctypes.byref(cp), ctypes.byref(cb), fake,
+                                           w.num_q_heads, w.sm_scale, fake, None)
+    assert rc == echo.ECHO_E_WORKSPACE
+    assert "static scratch holds 33554432" in echo.last_error()
