@@ -6,12 +6,20 @@ stream: copy-on-write block copies, KV append, then mixed attention (prefill
 chunks, decode split-KV with shared prefixes read once, merge).  Inputs are
 resident in HBM before the timed region.  Prints one JSON line.
 
-    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 2]
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--config 4] [--configs 1,2,3,4,5]
 
-`value` is query tokens per second of whole steps.  The roofline object is
-for the step's dominant kernel, timed with HIP events that the library
-records around each launch on the same stream (echo_profile), over K more
-steps after the timed ones.
+The headline workload (`--config`, default 4: the long-context prefix-shared
+mixed batch, the largest of the five) gives `value` (query tokens per second
+of whole steps), `ms_per_step`, the roofline of its dominant kernel and the
+CPU baseline.  `per_config` repeats the measurement for every configuration
+in `--configs`: tokens/s, decode HBM GB/s and prefill MFMA TFLOP/s each
+against its peak, the whole-iteration fraction max(bytes / 8 TB/s, FLOPs /
+2.5 PFLOP/s) / step time, and the max abs error of that run's outputs against
+the fp64 oracle (every output for configurations 1-3; every decode output and
+whole prefill tiles for 4 and 5, where the full oracle takes minutes).
+Kernel times come from HIP events that the library records around each
+launch on the same stream (echo_profile), over K more steps after the timed
+ones.
 """
 from __future__ import annotations
 
@@ -52,7 +60,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
-    ap.add_argument("--config", type=int, default=2, choices=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--config", type=int, default=4, choices=[1, 2, 3, 4, 5, 6])
+    ap.add_argument("--configs", default="1,2,3,4,5",
+                    help="configurations measured for per_config ('' for none)")
+    ap.add_argument("--config-steps", type=int, default=10,
+                    help="timed steps per configuration in per_config")
+    ap.add_argument("--no-error-check", action="store_true")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-threads", type=int, default=0)
     ap.add_argument("--copy-pairs", type=int, default=1024)
@@ -90,10 +103,10 @@ def cpu_baseline(w, threads):
     """The fp64 oracle on the host cores: the whole iteration when it fits the
     budget, else a bounded sample of query vectors (stated in the record)."""
     import oracle
-    from tests.gpu_util import compact
+    from tests.gpu_util import compact, oracle_pool
     c, _ = compact(w)
     t0 = time.perf_counter()
-    pool = oracle.prepare(c)
+    pool = oracle_pool(c, threads)
     t_prep = time.perf_counter() - t0
     t0 = time.perf_counter()
     if c.cow_pairs.shape[0]:
@@ -104,7 +117,7 @@ def cpu_baseline(w, threads):
     q = np.diff(c.batch.q_start)
     klim = np.concatenate([c.batch.seq_lens[r] - q[r] + 1 + np.arange(q[r])
                            for r in range(c.batch.num_rows)])
-    budget_keys = 1.5e8 * threads    # roughly 10-20 s of fp64 work
+    budget_keys = 5e7 * threads    # roughly 10-20 s of fp64 work
     total_keys = float(klim.sum()) * Hq
     if total_keys <= budget_keys:
         sel, frac, what = None, 1.0, "all query vectors"
@@ -209,55 +222,68 @@ def layer_bench(args):
     return 0
 
 
-def main():
-    args = parse()
-    if args.layer and args.gpus == 1:
-        return layer_bench(args)
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the hot path "
-              "shards by KV head or by prefix group with no exchange, but this build runs on a "
-              "single MI355X.", file=sys.stderr)
-        return 2
+def host_info() -> dict:
+    """Host CPUs of this process: nproc, affinity, cgroup quota, model."""
+    from tests.gpu_util import cpu_share
+    model = ""
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
+    quota = None
+    try:
+        with open("/sys/fs/cgroup/cpu.max") as f:
+            q, per = f.read().split()[:2]
+            quota = None if q == "max" else round(int(q) / int(per), 2)
+    except (OSError, ValueError):
+        pass
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)),
+            "cgroup_cpu_quota": quota, "threads_used": cpu_share(), "cpu_model": model}
+
+
+def measure(cfg, steps, warmup, check_error, threads):
+    """One configuration: whole-step time, per-kernel times, algorithmic
+    bytes and FLOPs, rooflines and (optionally) the max abs error against the
+    oracle.  Returns (entry, internals)."""
     import torch
     from paper_2504_03651_amd import echo
     from paper_2504_03651_amd import workload as W
     from paper_2504_03651_amd.session import Iteration
 
-    echo.lib()
     t0 = time.perf_counter()
-    w = W.config(args.config)
-    log(f"[bench] generated {w.name} in {time.perf_counter() - t0:.1f} s")
+    w = W.config(cfg)
+    log(f"[bench] cfg{cfg}: generated {w.name} in {time.perf_counter() - t0:.1f} s")
     it = Iteration(w)
     torch.cuda.synchronize()
-    log("[bench] pool built on device")
     cp, cb, _ = echo.host_structs(w)
     st = echo.plan_stats(cp, cb, w.num_q_heads)
-
-    for _ in range(args.warmup):
+    for _ in range(warmup):
         it.step()
     torch.cuda.synchronize()
-    log(f"[bench] {args.warmup} warmup steps done")
 
-    # ---- timed steps
     stream = torch.cuda.current_stream()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record(stream)
     t_host = time.perf_counter()
-    for _ in range(args.steps):
+    for _ in range(steps):
         it.step()
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_host
-    ms = start.elapsed_time(stop) / args.steps
-    log(f"[bench] {args.steps} steps: {ms:.4f} ms/step (host wall {wall / args.steps * 1e3:.4f})")
+    ms = start.elapsed_time(stop) / steps
+    log(f"[bench] cfg{cfg}: {steps} steps {ms:.4f} ms/step (host wall {wall / steps * 1e3:.4f})")
 
-    # ---- per-kernel times, HIP events recorded by the library on this stream
-    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(args.steps)]
+    # per-kernel times: HIP events the library records on this stream
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(3)] for _ in range(steps)]
     timings = []
     echo.profile(True)
-    for k in range(args.steps):
+    for k in range(steps):
         ev[k][0].record(stream)
         it.copy()
         ev[k][1].record(stream)
@@ -273,15 +299,96 @@ def main():
     # kernel times are in the rocprofv3 summaries
     kms["block_copy_call_ms"] = float(np.mean([e[0].elapsed_time(e[1]) for e in ev]))
     kms["kv_append_call_ms"] = float(np.mean([e[1].elapsed_time(e[2]) for e in ev]))
-    log("[bench] per-kernel ms: " + ", ".join(f"{k} {v:.4f}" for k, v in kms.items()))
+    log(f"[bench] cfg{cfg}: per-kernel ms: " + ", ".join(f"{k} {v:.4f}" for k, v in kms.items()))
 
-    # ---- roofline of the dominant kernel
     T, Hq, Hkv, D = w.batch.num_tokens, w.num_q_heads, w.num_kv_heads, w.head_dim
     eb = w.kv_bytes_per_elem()
     kv_tok = 2 * D * eb + (2 * 4 / 16 if eb == 1 else 0)   # K+V bytes per token per KV head
     n_dec = int((w.batch.row_kind == W.DECODE).sum())
     dec_bytes = st["decode_kv_tokens"] * Hkv * kv_tok + n_dec * Hq * D * (2 + 4)
     pf_flops = 4.0 * Hq * D * st["prefill_causal_pairs"]
+    # whole step: decode bytes + the append (new K/V read as bf16, written as
+    # codes) + copy-on-write pairs (read + write whole blocks), against FLOPs
+    app_bytes = T * Hkv * D * 2 * (2 + eb)
+    cow_bytes = int(w.cow_pairs.shape[0]) * 2 * 2 * Hkv * 16 * D * eb
+    step_bytes = dec_bytes + app_bytes + cow_bytes
+    t_roof = max(step_bytes / (HBM_PEAK_GBS * 1e9), pf_flops / (BF16_PEAK_TFLOPS * 1e12))
+    entry = {"workload": f"{w.name}: {DESCRIPTIONS[cfg]}", "rows": w.batch.num_rows,
+             "query_tokens": T, "kv_dtype": w.kv_dtype, "ms_per_step": round(ms, 4),
+             "tokens_per_s": round(T / (ms * 1e-3), 1),
+             "whole_iteration_frac": round(t_roof / (ms * 1e-3), 4),
+             "roofline_step_ms": round(t_roof * 1e3, 4),
+             "kernels_ms": {k: round(v, 4) for k, v in kms.items()}}
+    if kms["decode_ms"] > 0:
+        gbs = dec_bytes / (kms["decode_ms"] * 1e-3) / 1e9
+        entry["decode"] = {"GBps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
+                           "algorithmic_bytes": int(dec_bytes), "ms": round(kms["decode_ms"], 4)}
+    if kms["prefill_ms"] > 0:
+        tf = pf_flops / (kms["prefill_ms"] * 1e-3) / 1e12
+        entry["prefill"] = {"TFLOPs": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
+                            "algorithmic_flops": int(pf_flops), "ms": round(kms["prefill_ms"], 4)}
+    if check_error:
+        entry["max_abs_err"] = oracle_error(w, it, cfg, threads)
+    internals = {"w": w, "it": it, "kms": kms, "st": st, "dec_bytes": dec_bytes,
+                 "pf_flops": pf_flops, "ms": ms}
+    return entry, internals
+
+
+def oracle_error(w, it, cfg, threads):
+    """Max abs error of this run's outputs against the fp64 oracle (and the
+    pool bit for bit on the blocks the batch touches)."""
+    import oracle
+    from tests.gpu_util import compact, oracle_pool, tile_queries
+    t0 = time.perf_counter()
+    out = it.out.cpu().numpy().reshape(-1, w.head_dim).astype(np.float64)
+    c, ids = compact(w)
+    pool = oracle_pool(c, threads)
+    # the pool after the timed steps equals one iteration's: the copy and the
+    # append write the same bytes every step
+    if c.cow_pairs.shape[0]:
+        oracle.block_copy(pool, c.cow_pairs)
+    oracle.kv_append(pool, c.batch, c.k_new, c.v_new)
+    k, v, ks, vs = it.pool_host(ids)
+    pool_ok = bool(np.array_equal(k, pool.k) and np.array_equal(v, pool.v))
+    if pool.fp8:
+        pool_ok = pool_ok and bool(np.array_equal(ks.view(np.uint32), pool.k_scale.view(np.uint32))
+                                   and np.array_equal(vs.view(np.uint32),
+                                                      pool.v_scale.view(np.uint32)))
+    sel = None if cfg in (1, 2, 3) else tile_queries(w)
+    ref = oracle.attention(pool, c.batch, c.q, c.num_q_heads, c.sm_scale, sel=sel,
+                           threads=threads)
+    got = out if sel is None else out[sel]
+    err = float(np.abs(got - ref).max()) if ref.size else 0.0
+    n = out.shape[0]
+    what = "all" if sel is None else f"{len(sel)} of {n} (every decode output, whole prefill tiles)"
+    log(f"[bench] cfg{cfg}: oracle check over {what} query vectors: max abs err {err:.3e}, "
+        f"pool {'bit-exact' if pool_ok else 'DIFFERS'} ({time.perf_counter() - t0:.1f} s)")
+    return {"value": err, "query_vectors": what, "pool_bit_exact": pool_ok}
+
+
+def main():
+    args = parse()
+    if args.layer and args.gpus == 1:
+        return layer_bench(args)
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the hot path "
+              "shards by KV head or by prefix group with no exchange, but this build runs on a "
+              "single MI355X.", file=sys.stderr)
+        return 2
+    import torch
+    from paper_2504_03651_amd import echo
+
+    echo.lib()
+    hi = host_info()
+    threads = args.cpu_threads or hi["threads_used"]
+    log(f"[bench] host: {hi}")
+    configs = [int(x) for x in args.configs.split(",") if x.strip()]
+
+    # ---- the headline workload
+    head, inner = measure(args.config, args.steps, args.warmup, not args.no_error_check,
+                          threads)
+    w, it, kms = inner["w"], inner["it"], inner["kms"]
+    dec_bytes, pf_flops = inner["dec_bytes"], inner["pf_flops"]
     if kms["decode_ms"] >= kms["prefill_ms"]:
         t_k = kms["decode_ms"] * 1e-3
         achieved = dec_bytes / t_k / 1e9
@@ -299,32 +406,56 @@ def main():
                 "kernel": "prefill_kernel (bf16 MFMA, causal chunks)",
                 "algorithmic_flops": int(pf_flops), "avg_ms": round(kms["prefill_ms"], 4)}
     side = {}
-    if kms["decode_ms"] > 0:
-        side["decode_GBps"] = round(dec_bytes / (kms["decode_ms"] * 1e-3) / 1e9, 1)
-        side["decode_frac_hbm"] = round(side["decode_GBps"] / HBM_PEAK_GBS, 4)
-    if kms["prefill_ms"] > 0:
-        side["prefill_TFLOPs"] = round(pf_flops / (kms["prefill_ms"] * 1e-3) / 1e12, 1)
-        side["prefill_frac_mfma"] = round(side["prefill_TFLOPs"] / BF16_PEAK_TFLOPS, 4)
-
-    rec = {"metric": METRIC, "value": round(T / (ms * 1e-3), 1), "unit": "tokens/s",
+    if "decode" in head:
+        side["decode"] = dict(head["decode"], bound="hbm", peak=HBM_PEAK_GBS, unit="GB/s",
+                              kernel="attn_kernel",
+                              traffic=measured_traffic(args.config, "attn_kernel"))
+    if "prefill" in head:
+        side["prefill"] = dict(head["prefill"], bound="mfma", peak=BF16_PEAK_TFLOPS,
+                               unit="TFLOP/s", kernel="prefill_kernel",
+                               traffic=measured_traffic(args.config, "prefill_kernel"))
+    eb = w.kv_bytes_per_elem()
+    T = w.batch.num_tokens
+    rec = {"metric": METRIC, "value": head["tokens_per_s"], "unit": "tokens/s",
            "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
-           "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+           "ms_per_step": head["ms_per_step"], "higher_is_better": True, "scaling": "weak",
            "vs_baseline": None, "dtype": "bf16" if eb == 2 else "bf16 (fp8-e4m3 KV)",
            "data": "synthetic",
-           "config": {"workload": f"{w.name}: {DESCRIPTIONS[args.config]}",
-                      "rows": w.batch.num_rows, "query_tokens": T, "q_heads": Hq,
-                      "kv_heads": Hkv, "head_dim": D, "pool_blocks": w.num_blocks,
-                      "cow_pairs": int(w.cow_pairs.shape[0])},
+           "config": {"workload": head["workload"], "rows": w.batch.num_rows,
+                      "query_tokens": T, "q_heads": w.num_q_heads,
+                      "kv_heads": w.num_kv_heads, "head_dim": w.head_dim,
+                      "pool_blocks": w.num_blocks, "cow_pairs": int(w.cow_pairs.shape[0])},
            "roofline": roof,
-           "kernels_ms": {k: round(v, 4) for k, v in kms.items()},
-           "side_rooflines": side,
-           "plan": st}
+           "rooflines": side,
+           "whole_iteration_frac": head["whole_iteration_frac"],
+           "kernels_ms": head["kernels_ms"],
+           "plan": inner["st"]}
+    if "max_abs_err" in head:
+        rec["max_abs_err"] = head["max_abs_err"]
     if args.copy_pairs > 0:
         rec["block_copy_bench"] = copy_benchmark(it, w, args.copy_pairs)
     if not args.no_cpu_baseline:
-        threads = args.cpu_threads or min(16, os.cpu_count() or 1)
         log(f"[bench] timing the oracle on {threads} host threads")
-        rec["cpu_baseline"] = cpu_baseline(w, threads)
+        cb = cpu_baseline(w, threads)
+        cb.update({k: hi[k] for k in ("nproc", "affinity", "cgroup_cpu_quota", "cpu_model")})
+        rec["cpu_baseline"] = cb
+    del it, inner
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+    # ---- every configuration
+    per = {}
+    for cfg in configs:
+        if cfg == args.config:
+            per[f"cfg{cfg}"] = head
+            continue
+        e, inn = measure(cfg, args.config_steps, args.warmup, not args.no_error_check, threads)
+        per[f"cfg{cfg}"] = e
+        del inn
+        torch.cuda.synchronize()
+        torch.cuda.empty_cache()
+    if per:
+        rec["per_config"] = per
     print(json.dumps(rec), flush=True)
     return 0
 
