@@ -1,4 +1,9 @@
-"""Builds libecho.so in-tree with hipcc for gfx950 (no JIT, no cache)."""
+"""Builds libecho.so in-tree with hipcc for gfx950 (no JIT, no cache).
+
+``build_sanitized()`` builds a copy whose host code (the planner, the block
+manager and the validation in the C ABI) carries AddressSanitizer and
+UndefinedBehaviorSanitizer instrumentation, for running the host-only tests
+under them on a CPU; the device code is built as usual."""
 from __future__ import annotations
 
 import os
@@ -41,6 +46,48 @@ def build(verbose: bool = False) -> str:
         raise RuntimeError("link of libecho.so failed")
     os.replace(tmp, OUT)
     return OUT
+
+
+# host sources instrumented by build_sanitized(); the others keep device code
+SANITIZED = ("plan.cpp", "abi.cpp", "kvm.cpp")
+SAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+             "-fno-sanitize-recover=all", "-fno-omit-frame-pointer", "-g"]
+
+
+def sanitizer_runtime() -> str:
+    """The clang AddressSanitizer runtime that a sanitized build needs
+    preloaded into an uninstrumented interpreter."""
+    import glob
+    hits = sorted(glob.glob("/opt/rocm/llvm/lib/clang/*/lib/linux/libclang_rt.asan-x86_64.so"))
+    if not hits:
+        raise RuntimeError("clang AddressSanitizer runtime not found under /opt/rocm/llvm")
+    return hits[-1]
+
+
+def build_sanitized(out: str | None = None, verbose: bool = False) -> str:
+    out = out or os.path.join(ROOT, "_build", "san", "libecho_san.so")
+    bdir = os.path.dirname(out)
+    os.makedirs(bdir, exist_ok=True)
+    objs = []
+    for src in SOURCES:
+        obj = os.path.join(bdir, src + ".o")
+        extra = SAN_FLAGS if src in SANITIZED else []
+        cmd = [HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
+        if verbose:
+            print(" ".join(cmd), flush=True)
+        r = subprocess.run(cmd, capture_output=True, text=True)
+        if r.returncode != 0:
+            sys.stderr.write(r.stdout + r.stderr)
+            raise RuntimeError(f"hipcc failed on {src} (sanitized build)")
+        objs.append(obj)
+    cmd = [HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", "-Xarch_host", "-fsanitize=address",
+           "-Xarch_host", "-fsanitize=undefined", "-shared-libsan", "-o", out, *objs,
+           "-L/opt/rocm/lib", "-lhipblaslt", "-Wl,-rpath,/opt/rocm/lib"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        sys.stderr.write(r.stdout + r.stderr)
+        raise RuntimeError("link of the sanitized libecho failed")
+    return out
 
 
 if __name__ == "__main__":

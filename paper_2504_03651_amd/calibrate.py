@@ -4,7 +4,9 @@
 
 Times one iteration of the library (``echo_kv_append`` + ``echo_attn_mixed``)
 with events on the current stream for:
-  * prefill-only batches: one request of l new tokens, no cached context;
+  * prefill-only batches: one request of l new tokens, no cached context,
+    and batches of several chunks (up to 32k new tokens, some after cached
+    context), so that the quadratic term is measured where the GPU is full;
   * decode-only batches: n requests with lengths drawn from several shapes
     (uniform, one long row among short ones, equal lengths);
   * mixed batches: one prefill request next to a decode batch, together with
@@ -55,13 +57,22 @@ def _w(rows, cfg, seed):
                    seed=seed)
 
 
+# prefill batches: (number of chunks, new tokens each, cached context each)
+PREFILL_BATCHES = [(1, l, 0) for l in (16, 64, 256, 512, 1024, 2048, 3072, 4096, 6144, 8192,
+                                       12288, 16384)] + [
+    (2, 4096, 0), (4, 2048, 0), (4, 4096, 0), (8, 2048, 0), (8, 4096, 0), (2, 8192, 0),
+    (4, 8192, 0), (16, 1024, 0), (16, 2048, 0), (3, 3072, 0), (6, 1536, 0), (12, 1024, 0),
+    (1, 2048, 8192), (1, 2048, 16384), (1, 4096, 16384), (2, 4096, 8192), (4, 2048, 4096),
+    (4, 4096, 4096), (8, 1024, 8192), (2, 1024, 30000)]
+
+
 def samples(cfg, reps, log=print):
     rng = np.random.default_rng(cfg.get("seed", 0))
     pre = []
-    for l in (16, 32, 64, 128, 256, 512, 768, 1024, 1536, 2048, 3072, 4096, 6144, 8192):
-        t = _time(_w([W.RowSpec(W.PREFILL, 0, l)], cfg, l), reps)
-        pre.append((l, t))
-        log(f"prefill l={l}: {t:.4f} ms")
+    for k, l, c in PREFILL_BATCHES:
+        t = _time(_w([W.RowSpec(W.PREFILL, c, l)] * k, cfg, l + k), reps)
+        pre.append(([(l, c)] * k, t))
+        log(f"prefill {k} x l={l} after {c}: {t:.4f} ms")
     dec = []
     for n in (16, 64, 256):
         # lengths up to about 300k cached tokens per batch (host draws stay small)
@@ -101,7 +112,12 @@ def fit_and_score(pre, dec, mix, cfg, seed=0):
         return np.sort(idx[:k]), np.sort(idx[k:])
 
     pi, po = split(len(pre))
-    pm = PrefillModel.fit([pre[i][0] for i in pi], [pre[i][1] for i in pi])
+    pm = PrefillModel.fit_chunks([pre[i][0] for i in pi], [pre[i][1] for i in pi])
+    # the paper's own reading, one prompt at a time: single prompts only
+    single = [i for i in range(len(pre)) if len(pre[i][0]) == 1 and pre[i][0][0][1] == 0]
+    si = [i for i in single if i in set(pi.tolist())]
+    so = [i for i in single if i not in set(pi.tolist())]
+    pm_single = PrefillModel.fit([pre[i][0][0][0] for i in si], [pre[i][1] for i in si])
     # decode: hold out one sample of each batch size and shape group at random
     di, do = split(len(dec))
     dm_paper = DecodeModel.fit([dec[i][0] for i in di], [dec[i][1] for i in di])
@@ -122,8 +138,11 @@ def fit_and_score(pre, dec, mix, cfg, seed=0):
         return abs(pred - t) / t
 
     report = {
-        "prefill_heldout": [(pre[i][0], pre[i][1], float(pm.predict(pre[i][0])))
-                            for i in po],
+        "prefill_heldout": [(len(pre[i][0]), pre[i][0][0][0], pre[i][0][0][1], pre[i][1],
+                             pm.predict_chunks(pre[i][0])) for i in po],
+        "prefill_heldout_single_prompt_fit": [(1, pre[i][0][0][0], 0, pre[i][1],
+                                               float(pm_single.predict(pre[i][0][0][0])))
+                                              for i in so],
         "decode_heldout_paper_form": [(len(dec[i][0]), int(max(dec[i][0])),
                                        float(np.mean(dec[i][0])), dec[i][1],
                                        dm_paper.predict(dec[i][0])) for i in do],
@@ -137,7 +156,8 @@ def fit_and_score(pre, dec, mix, cfg, seed=0):
     errs["mixed_heldout_given_parts_sum_form"] = mixed_err(mm_sum)
     # the max term's share of the decode time (split-KV should keep it small)
     share = [dm.coef(len(b))[0] * max(b) / dm.predict(b) for b, _ in dec]
-    est.config = dict(cfg, decode_paper_form=dm_paper.__dict__, mixed_paper_form=mm_paper.__dict__)
+    est.config = dict(cfg, decode_paper_form=dm_paper.__dict__, mixed_paper_form=mm_paper.__dict__,
+                      prefill_single_prompt_fit=pm_single.__dict__)
     return est, report, errs, float(np.mean(share))
 
 
@@ -151,7 +171,11 @@ def markdown(out, command):
              "Times are the GPU time of one iteration of the library (KV append + attention; "
              "host planning excluded), median of the repetitions, events on the stream.", "",
              f"* prefill T = max(alpha l^2 + beta l, c): alpha = {p['alpha']:.4g} ms, "
-             f"beta = {p['beta']:.4g} ms, c = {p['c']:.4g} ms",
+             f"beta = {p['beta']:.4g} ms, c = {p['c']:.4g} ms (fitted on batches of chunks, "
+             f"priced as alpha sum(n^2 + 2 n ctx) + beta sum(n)); fitted on single prompts "
+             f"only: alpha = {c['config']['prefill_single_prompt_fit']['alpha']:.4g}, beta = "
+             f"{c['config']['prefill_single_prompt_fit']['beta']:.4g}, c = "
+             f"{c['config']['prefill_single_prompt_fit']['c']:.4g}",
              "* decode T = gamma max(L) + delta mean(L) + eps, per batch size n:", ""]
     lines += ["| n | gamma (ms/token) | delta (ms/token) | eps (ms) |", "|---|---|---|---|"]
     for i, n in enumerate(d["sizes"]):
@@ -164,8 +188,9 @@ def markdown(out, command):
               "| model | error |", "|---|---|"]
     for k, v in e.items():
         lines.append(f"| {k} | {v:.3f} |")
-    lines += ["", "Samples (ms):", "", "| prefill l | time |", "|---|---|"]
-    lines += [f"| {l} | {t:.4f} |" for l, t in out["samples"]["prefill"]]
+    lines += ["", "Samples (ms):", "", "| prefill chunks | new tokens each | cached each | time |",
+              "|---|---|---|---|"]
+    lines += [f"| {len(b)} | {b[0][0]} | {b[0][1]} | {t:.4f} |" for b, t in out["samples"]["prefill"]]
     lines += ["", "| decode n | max L | mean L | time |", "|---|---|---|---|"]
     lines += [f"| {len(b)} | {max(b)} | {sum(b) / len(b):.0f} | {t:.4f} |"
               for b, t in out["samples"]["decode"]]

@@ -13,7 +13,9 @@ import os
 import numpy as np
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "libecho.so")
+# ECHO_LIBRARY selects another build of the library (the sanitized one of
+# build.build_sanitized(), for the host-only tests)
+LIB_PATH = os.environ.get("ECHO_LIBRARY") or os.path.join(_PKG, "libecho.so")
 
 ECHO_OK = 0
 ECHO_E_INVALID = -1

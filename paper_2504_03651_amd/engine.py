@@ -4,8 +4,8 @@ An ``AttentionEngine`` owns a device KV pool of the simulator's block count and
 executes each iteration's batch exactly as the simulator's KV block manager
 lays it out: its block tables and sequence lengths become the rows of an
 ``echo_kv_append`` + ``echo_attn_mixed`` call (prefill chunks and decode
-tokens, with seeded N(0, 1) bf16 Q/K/V for the new tokens; there is no
-model), so the manager's tables, evictions and prefix hits all reach the
+tokens, with seeded N(0, 1) bf16 Q/K/V for the new tokens, drawn on the
+device; there is no model), so the manager's tables, evictions and prefix hits all reach the
 kernels.  The GPU time of each call (host planning excluded) is measured with
 events on the stream, to set against the estimator's prediction for the same
 batch.
@@ -23,22 +23,29 @@ BS = 16
 
 class AttentionEngine:
     def __init__(self, num_blocks: int, num_q_heads: int = 32, num_kv_heads: int = 8,
-                 head_dim: int = 128, seed: int = 0, device: str = "cuda"):
+                 head_dim: int = 128, seed: int = 0, device: str = "cuda", observer=None):
         import torch
         self.torch = torch
         self.Hq, self.Hkv, self.D = num_q_heads, num_kv_heads, head_dim
         self.pool = echo.KVPool(num_blocks, num_kv_heads, head_dim, False, device).poison()
-        self.rng = np.random.default_rng(seed)
+        self.gen = torch.Generator(device=device)
+        self.gen.manual_seed(seed)
         self.device = device
         self.ws = None
         self.ev = [torch.cuda.Event(enable_timing=True) for _ in range(2)]
         self.calls = 0
         self.gate_cycles = GATE_CYCLES
+        # optional: called after each batch as observer(engine, manager, batch,
+        # rows, q, k_new, v_new, out) with the host inputs (rows: a
+        # workload.Batch; q, k_new, v_new: bf16 bits) and the device output,
+        # for checking the results outside the product path
+        self.observer = observer
 
     def _bf16(self, shape):
-        x = self.rng.standard_normal(shape, dtype=np.float32)
-        u = x.view(np.uint32)
-        return ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+        """Seeded N(0, 1) values rounded to bf16, drawn on the device (int16 bits)."""
+        torch = self.torch
+        x = torch.randn(shape, generator=self.gen, device=self.device, dtype=torch.float32)
+        return x.to(torch.bfloat16).view(torch.int16)
 
     def __call__(self, manager, batch) -> float:
         """Runs one batch (list of (request, "prefill" | "decode", new tokens))
@@ -69,10 +76,9 @@ class AttentionEngine:
         kind = np.array([W.PREFILL if k == "prefill" else W.DECODE for r, k, n in batch], np.uint8)
         b = W.Batch(bt, sl, np.concatenate([[0], np.cumsum(q)]).astype(np.int32), kind)
         T = int(q.sum())
-        dev = lambda a: torch.from_numpy(a.view(np.int16)).to(self.device)
-        qd = dev(self._bf16((T, self.Hq, self.D)))
-        kd = dev(self._bf16((T, self.Hkv, self.D)))
-        vd = dev(self._bf16((T, self.Hkv, self.D)))
+        qd = self._bf16((T, self.Hq, self.D))
+        kd = self._bf16((T, self.Hkv, self.D))
+        vd = self._bf16((T, self.Hkv, self.D))
         db = echo.DeviceBatch(b, self.device)
         n = echo.workspace_bytes(self.pool, db, self.Hq)
         if self.ws is None or self.ws.numel() < n:
@@ -89,4 +95,8 @@ class AttentionEngine:
         torch.cuda.synchronize()
         self.calls += 1
         self.last_out = out_t
-        return float(self.ev[0].elapsed_time(self.ev[1]))
+        ms = float(self.ev[0].elapsed_time(self.ev[1]))
+        if self.observer is not None:
+            host = lambda t: t.cpu().numpy().view(np.uint16)
+            self.observer(self, manager, batch, b, host(qd), host(kd), host(vd), out_t)
+        return ms

@@ -77,6 +77,37 @@ class PrefillModel:
         return best[1]
 
 
+    def predict_chunks(self, chunks):
+        """A batch of prefill chunks (n new tokens after ctx cached ones) in
+        one launch: the work terms add and the floor applies once (a chunk
+        has n ctx + n^2 / 2 (query, key) pairs, priced at 2 alpha each, which
+        is alpha l^2 for a whole prompt of l tokens)."""
+        work = sum(self.alpha * (n * n + 2.0 * n * c) + self.beta * n for n, c in chunks)
+        return max(float(work), self.c)
+
+    @classmethod
+    def fit_chunks(cls, batches, t):
+        """As fit(), from batches of prefill chunks [(n, ctx), ...] priced by
+        predict_chunks: several chunks per batch make alpha identifiable on
+        GPUs where one prompt of a few thousand tokens does not fill the
+        machine (its time then grows about linearly)."""
+        t = np.asarray(t, np.float64)
+        q = np.array([sum(n * n + 2.0 * n * c for n, c in b) for b in batches], np.float64)
+        l = np.array([sum(n for n, _c in b) for b in batches], np.float64)
+        best = None
+        for c in np.unique(np.concatenate([[0.0], t])):
+            m = t > c
+            if m.sum() < 2:
+                continue
+            a, b = _nnls2(q[m] / t[m], l[m] / t[m], np.ones(int(m.sum())))
+            mdl = cls(a, b, float(c))
+            pred = np.array([mdl.predict_chunks(x) for x in batches])
+            err = float(np.sum(((pred - t) / t) ** 2))
+            if best is None or err < best[0]:
+                best = (err, mdl)
+        return best[1]
+
+
 @dataclass
 class DecodeModel:
     """gamma, delta (and eps) per batch size; coefficients interpolate linearly

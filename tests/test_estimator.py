@@ -100,3 +100,17 @@ def test_kernel_reading_of_the_forms():
     # shared prefix blocks read once: the mean term takes distinct tokens per row
     g, d, e = est.decode.coef(16)
     assert est.batch_time_kernel([], L, 1000) == pytest.approx(g * 400 + d * 1000 / 16 + e)
+
+
+def test_prefill_fit_on_batches_of_chunks_recovers_known_coefficients():
+    # several chunks per batch, some after cached context, priced by the
+    # kernel reading: alpha sum(n^2 + 2 n ctx) + beta sum(n), floor once
+    from paper_2504_03651_amd.calibrate import PREFILL_BATCHES
+    alpha, beta, c = 3.0e-9, 2.0e-5, 0.025
+    batches = [[(l, ctx)] * k for k, l, ctx in PREFILL_BATCHES]
+    t = [max(sum(alpha * (n * n + 2 * n * x) + beta * n for n, x in b), c) for b in batches]
+    m = PrefillModel.fit_chunks(batches, t)
+    assert m.alpha == pytest.approx(alpha, rel=1e-6) and m.beta == pytest.approx(beta, rel=1e-6)
+    assert m.c == pytest.approx(c)
+    # one prompt of l tokens from scratch is the paper's alpha l^2 + beta l
+    assert m.predict_chunks([(4096, 0)]) == pytest.approx(float(m.predict(4096)))
