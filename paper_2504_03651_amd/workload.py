@@ -378,14 +378,15 @@ def config4(seed: int = 4, **kw) -> Workload:
     return build("cfg4-long-context", rows, groups, 64, 8, 128, seed=seed, **kw)
 
 
-def config5(seed: int = 5, **kw) -> Workload:
+def config5(seed: int = 5, kv_dtype: str = KV_FP8, **kw) -> Workload:
     """Configuration 3 at four times the batch (32 online decode rows, two
     2048-token prefill chunks, 512 offline decode rows in 16 groups of 32) with
     the KV cache stored as fp8-e4m3 and one fp32 scale per block per KV head
-    for K and for V."""
+    for K and for V.  ``kv_dtype=KV_BF16`` gives the same values in a bf16
+    cache (the unquantised twin)."""
     g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, 0])))
     rows, groups = _mixed_rows(g, 32, 2, 512, 32)
-    return build("cfg5-mixed-fp8", rows, groups, 32, 8, 128, kv_dtype=KV_FP8, seed=seed, **kw)
+    return build("cfg5-mixed-fp8", rows, groups, 32, 8, 128, kv_dtype=kv_dtype, seed=seed, **kw)
 
 
 def late_chunk(seed: int = 6, **kw) -> Workload:

@@ -115,6 +115,36 @@ def test_fp8_queries_seeing_few_keys(torch_cuda):
     _check_small(w, torch_cuda, "fp8-few-keys")
 
 
+def _bf16_scaled(bits, factor):
+    """bf16 bit patterns of the values times a power of two (exact)."""
+    x = (bits.astype(np.uint32) << 16).view(np.float32) * np.float32(factor)
+    return (x.view(np.uint32) >> 16).astype(np.uint16)
+
+
+def test_fp8_prefill_values_near_the_fp16_range(torch_cuda):
+    # chunked prefill over an e4m3 pool carries V times its block scale in
+    # fp16: values up to the header's +-65504 stay finite.  V is N(0, 1) times
+    # 2^13 (largest |v| about 4e4), so outputs and their rounding scale by
+    # 2^13 as well: the bar is ATOL times that factor
+    rows = [W.RowSpec(W.PREFILL, 0, 200), W.RowSpec(W.PREFILL, 300, 64), W.RowSpec(W.DECODE, 500, 1),
+            W.RowSpec(W.PREFILL, 1000, 17)]
+    w = W.build("fp8-large-v", rows, {}, 16, 4, 128, kv_dtype=W.KV_FP8, seed=29)
+    f = 2.0 ** 13
+    w.v_new = _bf16_scaled(w.v_new, f)
+    w.ctx_v = _bf16_scaled(w.ctx_v, f)
+    vmax = float(np.abs((w.v_new.astype(np.uint32) << 16).view(np.float32)).max())
+    say(f"[case] fp8 prefill with |V| up to {vmax:.0f}")
+    assert 2.0e4 < vmax < 65504.0
+    it = _run(w, torch_cuda)
+    pool, ref = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    got = it.out.cpu().numpy().reshape(ref.shape)
+    assert np.isfinite(got).all()
+    err, nerr = attn_error(got, ref)
+    say(f"       max abs err {err:.3e} (bar {ATOL * f:.1f})  normalised {nerr:.3e}")
+    assert err <= ATOL * f
+
+
 def _rows_case(name, n_decode, prefill_q, kv, seed):
     g = np.random.Generator(np.random.PCG64(seed))
     rows = [W.RowSpec(W.DECODE, int(g.integers(0, 80)), 1, int(g.integers(-1, 2)))
