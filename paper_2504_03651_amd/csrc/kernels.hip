@@ -739,11 +739,14 @@ __global__ __launch_bounds__(256) void attn_kernel(AttnArgs a) {
 // K/V tiles of 64 keys live in a 3-stage LDS ring as bf16 (e4m3 caches: V as
 // fp16), shared by the eight waves; bf16 tiles are requested two tiles ahead:
 //   K  [64 keys][D]            16-byte chunk q of row r stored at q ^ kswz(r)
-//   V  [4 blocks][D][16 keys]  (the pool's block layout) with the two 16-byte
-//                              halves of row d swapped when bit 3 of d is set
+//   V  [4 blocks][D/16][2][16][8]  per block and 16 rows d of V^T, keys 0-7
+//                              of the 16 rows, then keys 8-15 (16 bytes each)
 // kswz maps the key-row bits that differ between the 16 lanes of an MFMA
 // operand read onto distinct chunks, so every 16-lane read of 16 bytes per
-// lane touches all 64 LDS banks once (and 8-lane reads 32 banks once).
+// lane touches all 64 LDS banks once; a 16-lane V operand read is 256
+// contiguous bytes.  (Rows of 32 bytes with the halves swapped on bit 3 of d
+// also spread 16 lanes over 64 banks, yet cost 4 bank-conflict cycles per
+// read on gfx950, measured with SQ_LDS_BANK_CONFLICT; this layout costs none.)
 // bf16 pools are copied global -> LDS directly (global_load_lds_dwordx4, no
 // staging registers); e4m3 pools go through registers and are widened on the
 // way in: K to bf16, V to fp16 after multiplication by its (block, head) scale
@@ -893,8 +896,10 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
         const int off = (wave * NJ + j) * 1024 + 16 * lane;   // byte offset in the K / V region
         const int r = off / (2 * D), q = ((off / 16) % CHUNKS) ^ kswz(r);
         k_off[j] = (r & 15) * D + 8 * q;
-        const int within = off % (32 * D);
-        const int d = within / 32, h = ((within / 16) & 1) ^ ((d >> 3) & 1);
+        // V: 16-byte unit u of the block's region holds keys 8h..8h+7 of row
+        // d = 16(u / 32) + u % 16, h = (u / 16) % 2
+        const int u = (off % (32 * D)) / 16;
+        const int d = 16 * (u >> 5) + (u & 15), h = (u >> 4) & 1;
         v_off[j] = d * 16 + 8 * h;
     }
     auto tile_id = [&](int kt) -> int { return lids[min(4 * (kt - kt0) + bsel, nblk - 1)]; };
@@ -949,11 +954,10 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
     // zero V of keys at or past key_end in the tile of buffer `buf`
     auto zero_tail = [&](int kt, int buf) {
         uint16_t *vl = (uint16_t *)(lds + buf * LD::STAGE + LD::KBYTES);
-        for (int e = tid; e < 4 * D * 2; e += kPfThreads) {  // 16-byte halves of all V rows
-            const int b = e / (2 * D), d = (e / 2) % D, ph = e & 1;
-            const int h = ph ^ ((d >> 3) & 1);
-            const int key = kPfKeys * kt + 16 * b + 8 * h;
-            uint16_t *dst = vl + (b * D + d) * 16 + 8 * ph;
+        for (int e = tid; e < 4 * D * 2; e += kPfThreads) {  // 16-byte units of the four blocks
+            const int b = e / (2 * D), u = e % (2 * D);
+            const int key = kPfKeys * kt + 16 * b + 8 * ((u >> 4) & 1);
+            uint16_t *dst = vl + b * 16 * D + 8 * u;
 #pragma unroll
             for (int x = 0; x < 8; ++x)
                 if (key + x >= key_end) dst[x] = 0;
@@ -1046,8 +1050,7 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
     };
     auto pv = [&](const uint8_t *vl, int ch, const PT (&pf)[2]) {
         __builtin_amdgcn_iglp_opt(1);   // as in qk
-        const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + c16 * 32 +
-                              16 * ((g4 & 1) ^ ((c16 >> 3) & 1));
+        const uint8_t *vrow = vl + (2 * ch + (g4 >> 1)) * (32 * D) + (g4 & 1) * 256 + c16 * 16;
 #pragma unroll
         for (int i = 0; i < NT; ++i) {
             const PT vf = *(const PT *)(vrow + i * 16 * 32);
