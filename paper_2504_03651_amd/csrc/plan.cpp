@@ -144,6 +144,11 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     std::vector<int32_t> &cnt = plan.cnt, &moff = plan.moff, &cursor = plan.cursor;
     cnt.assign((size_t)B, 0);
     auto n_splits = [&](const Segment &s) { return (s.j1 - s.j0 + split - 1) / split; };
+    int64_t n_waves = 0;
+    for (const Segment &s : segs)
+        n_waves += (int64_t)n_splits(s) * ((s.nrows + nt_max - 1) / nt_max) * plan.waves_per_desc;
+    const bool equal_pieces =
+        n_waves <= (int64_t)kEqualPieceGenerations * kDecodeWavesPerCu * opt.num_cus;
     for (const Segment &s : segs)
         for (int32_t k = 0; k < s.nrows; ++k) cnt[seg_rows[s.rows_off + k]] += n_splits(s);
 
@@ -178,8 +183,10 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
             plan.sibling_waves = (int32_t)std::max<int64_t>(
                 plan.sibling_waves, (s.nrows + nt_max - 1) / nt_max * wpd);
         plan.stats.decode_kv_tokens += s.key_end - kBlock * s.j0;
-        for (int32_t j = s.j0; j < s.j1; j += split) {
-            const int32_t jend = std::min(j + split, s.j1);
+        const int32_t ns = n_splits(s);
+        const int32_t step = equal_pieces ? (s.j1 - s.j0 + ns - 1) / ns : split;
+        for (int32_t j = s.j0; j < s.j1; j += step) {
+            const int32_t jend = std::min(j + step, s.j1);
             for (int32_t k0 = 0; k0 < s.nrows; k0 += nt_max) {
                 const int32_t ntk = std::min(nt_max, s.nrows - k0);
                 WorkDesc d;

@@ -277,3 +277,39 @@ def test_small_decode_batches_split_finer():
     lay5, words5 = _decode(w5)
     d5 = words5[lay5["off_desc"]:lay5["off_desc"] + 8 * lay5["n_desc"]].reshape(-1, 8)
     assert ((d5[:, 4] - d5[:, 3] + 15) // 16).max() == 96
+
+
+def _decode_pieces(w):
+    lay, words = _decode(w)
+    d = words[lay["off_desc"]:lay["off_desc"] + 8 * lay["n_desc"]].reshape(-1, 8)
+    return lay, d
+
+
+def test_equal_pieces_on_few_generation_launches():
+    # the mixed batch's decode waves fill 1.2 generations of the resident
+    # slots (12 waves x 256 CUs): a key range of n blocks cut into k pieces
+    # gets pieces of ceil(n / k) blocks (the last one shorter by less than k);
+    # the decode-only batch's 4.1 generations keep full 48-block pieces plus a
+    # remainder
+    for cfg, equal in ((3, True), (2, False)):
+        w = W.config(cfg, values=False)
+        lay, d = _decode_pieces(w)
+        waves = len(d) * w.num_kv_heads * lay["head_chunks"]
+        assert (waves <= 3 * 12 * 256) == equal
+        # pieces of one key range: same bt_row and slice, consecutive ranges
+        ranges = {}
+        for tok_off, shape, bt_row, kb, ke, *_ in d.tolist():
+            ranges.setdefault((bt_row, tok_off), []).append((kb, ke))
+        split_ranges = 0
+        for pieces in ranges.values():
+            pieces.sort()
+            if len(pieces) < 2:
+                continue
+            split_ranges += 1
+            nblk = [(ke - kb + 15) // 16 for kb, ke in pieces]
+            if equal:
+                assert len(set(nblk[:-1])) == 1 and 0 <= nblk[0] - nblk[-1] < len(nblk), nblk
+                assert nblk[0] == -(-sum(nblk) // len(nblk)), nblk
+            else:
+                assert all(n == 48 for n in nblk[:-1]), nblk
+        assert split_ranges > 10
