@@ -20,15 +20,29 @@ from tests.gpu_util import say
 pytestmark = pytest.mark.gpu
 
 
-@pytest.mark.parametrize("shape", [(256, 4, 2, 64, 512), (512, 8, 2, 128, 1024)])
+def _batch(shape):
+    H, Hq, Hkv, D, I = shape
+    if H < 4096:
+        return W.random_case(21, num_rows=7, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D,
+                             max_ctx=700, max_q=60)
+    # LLaMA-3.1-8B layer shapes (hidden 4,096, GQA 32/8, head_dim 128,
+    # intermediate 14,336): two prefill chunks, one on a 300-token context,
+    # and three decode rows, two of them sharing a 256-token prefix
+    rows = [W.RowSpec(W.PREFILL, 300, 40), W.RowSpec(W.DECODE, 500, 1, 0),
+            W.RowSpec(W.PREFILL, 0, 33), W.RowSpec(W.DECODE, 257, 1, 0),
+            W.RowSpec(W.DECODE, 129, 1)]
+    return W.build("layer-llama8b", rows, {0: 256}, Hq, Hkv, D, seed=24)
+
+
+@pytest.mark.parametrize("shape", [(256, 4, 2, 64, 512), (512, 8, 2, 128, 1024),
+                                   (4096, 32, 8, 128, 14336)])
 def test_layer_matches_the_oracle(shape):
     import torch
     from paper_2504_03651_amd import echo, layer
     from paper_2504_03651_amd.session import Iteration
     H, Hq, Hkv, D, I = shape
     lw = W.layer_weights(7, H, Hq, Hkv, D, I)
-    w = W.random_case(21, num_rows=7, num_q_heads=Hq, num_kv_heads=Hkv, head_dim=D, max_ctx=700,
-                      max_q=60)
+    w = _batch(shape)
     T = w.batch.num_tokens
     x = W.layer_hidden(8, T, H)
     say(f"[case] layer {shape}: {w.batch.num_rows} rows, {T} tokens")
