@@ -91,7 +91,7 @@ typedef struct {
     int32_t max_blocks_per_row;   /* row stride of block_tables */
     int32_t num_tokens;           /* T = q_start[B] */
     int32_t max_q_len;            /* >= every row's new-token count */
-    int32_t max_seq_len;          /* >= every seq_lens[r] */
+    int32_t max_seq_len;          /* >= every seq_lens[r]; at most 2^30 (else ECHO_E_UNSUPPORTED) */
     const int32_t *block_tables;  /* [B][max_blocks_per_row]; entry j holds positions
                                      16j..16j+15; entries at or past ceil(L/16) unused */
     const int32_t *seq_lens;      /* [B] L_r: cached tokens + this call's new tokens */

@@ -76,6 +76,8 @@ int check_batch(const echo_kv_pool_t *p, const echo_batch_t *b, bool for_append)
                                        b->num_tokens, B);
     if (b->max_q_len < 1 || b->max_seq_len < 1)
         return fail(ECHO_E_INVALID, "max_q_len / max_seq_len must be >= 1");
+    if (b->max_seq_len > kMaxSeqLen)
+        return fail(ECHO_E_UNSUPPORTED, "max_seq_len %d above %d", b->max_seq_len, kMaxSeqLen);
     if ((int64_t)b->max_seq_len > (int64_t)b->max_blocks_per_row * kBlock)
         return fail(ECHO_E_INVALID, "max_seq_len %d exceeds the block table width", b->max_seq_len);
     if (!b->block_tables || !b->seq_lens || !b->q_start || !b->row_kind)
@@ -88,17 +90,21 @@ int check_batch(const echo_kv_pool_t *p, const echo_batch_t *b, bool for_append)
         return fail(ECHO_E_INVALID, "q_start[num_rows] = %d != num_tokens %d", qs[B],
                     b->num_tokens);
     for (int32_t r = 0; r < B; ++r) {
-        const int32_t q = qs[r + 1] - qs[r], L = sl[r];
+        // differences of caller values in 64 bits: no overflow before the checks
+        const int64_t q = (int64_t)qs[r + 1] - qs[r], L = sl[r];
         const uint8_t kind = b->h_row_kind[r];
         if (kind != ECHO_ROW_DECODE && kind != ECHO_ROW_PREFILL)
             return fail(ECHO_E_INVALID, "row %d: kind %d", r, kind);
-        if (q < 1) return fail(ECHO_E_INVALID, "row %d: %d new tokens", r, q);
+        if (q < 1) return fail(ECHO_E_INVALID, "row %d: %lld new tokens", r, (long long)q);
         if (kind == ECHO_ROW_DECODE && q != 1)
-            return fail(ECHO_E_INVALID, "row %d: decode row with %d new tokens", r, q);
-        if (q > b->max_q_len) return fail(ECHO_E_INVALID, "row %d: q %d > max_q_len", r, q);
-        if (L < q) return fail(ECHO_E_INVALID, "row %d: seq_len %d < new tokens %d", r, L, q);
+            return fail(ECHO_E_INVALID, "row %d: decode row with %lld new tokens", r, (long long)q);
+        if (q > b->max_q_len)
+            return fail(ECHO_E_INVALID, "row %d: q %lld > max_q_len", r, (long long)q);
+        if (L < q)
+            return fail(ECHO_E_INVALID, "row %d: seq_len %lld < new tokens %lld", r, (long long)L,
+                        (long long)q);
         if (L > b->max_seq_len) return fail(ECHO_E_INVALID, "row %d: seq_len > max_seq_len", r);
-        const int32_t nb = (L + kBlock - 1) / kBlock;
+        const int32_t nb = (int32_t)((L + kBlock - 1) / kBlock);
         for (int32_t j = 0; j < nb; ++j) {
             const int32_t blk = bt[(size_t)r * b->max_blocks_per_row + j];
             if (blk < 0 || blk >= p->num_blocks)
@@ -135,7 +141,7 @@ int check_batch(const echo_kv_pool_t *p, const echo_batch_t *b, bool for_append)
         }
     }
     for (int32_t r = 0; r < B; ++r) {
-        const int32_t nb = (sl[r] + kBlock - 1) / kBlock;
+        const int32_t nb = (int32_t)(((int64_t)sl[r] + kBlock - 1) / kBlock);
         for (int32_t j = 0; j < nb; ++j) {
             const int32_t blk = bt[(size_t)r * b->max_blocks_per_row + j];
             if (stamp[blk] == epoch && (owner_row[blk] != r || owner_j[blk] != j))

@@ -17,6 +17,7 @@
 namespace echo {
 
 constexpr int kBlock = 16;
+constexpr int32_t kMaxSeqLen = 1 << 30;   // longest row accepted (key positions stay far from int overflow)
 constexpr int kWaveQueries = 16;   // query vectors per wave (MFMA N dimension)
 constexpr int kWavesPerGroup = 4;  // waves per workgroup
 

@@ -105,6 +105,22 @@ def test_q_start_must_start_at_zero_and_end_at_num_tokens():
     assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
 
 
+def test_extreme_q_start_and_lengths_are_rejected():
+    # caller values at the ends of int32: rejected by the checks, with no
+    # overflow on the way (the sanitized build runs this test too)
+    w = W.config1()
+    cp, cb, (bt, sl, qs, kd) = _structs(w)
+    qs[2] = -2**31            # q of row 1 negative, row 2 huge
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+    cp, cb, (bt, sl, qs, kd) = _structs(w)
+    sl[0] = 2**31 - 1          # beyond max_seq_len
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_INVALID
+    cp, cb, keep = _structs(w)
+    cb.max_seq_len = 2**30 + 1
+    cb.max_blocks_per_row = 2**27
+    assert echo.validate(cp, cb, False) == echo.ECHO_E_UNSUPPORTED
+
+
 def test_partial_mirrors_rejected():
     w = W.config1()
     cp, cb, keep = _structs(w)
