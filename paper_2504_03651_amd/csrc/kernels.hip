@@ -54,24 +54,43 @@ __device__ __forceinline__ bf16x8_t e4m3x8_to_bf16x8(u32x2_t w) {
     return (bf16x8_t){a[0], a[1], b[0], b[1], c[0], c[1], d[0], d[1]};
 }
 
-// fp32 -> OCP e4m3fn, round to nearest even, saturating to +-448.
+// fp32 -> OCP e4m3fn, round to nearest even, saturating to +-448, NaN to
+// 0x7F; without branches, so that the lanes of a wave do not diverge over
+// the value ranges.  Normal range (|y| >= 2^-6): round the bit pattern to 3
+// mantissa bits (a carry moves into the exponent), then rebias the exponent
+// (127 -> 7: minus 120 << 3); below it, steps of 2^-9 (|y| * 512 is exact).
 __device__ __forceinline__ uint32_t f32_to_e4m3(float y) {
     const uint32_t u = __float_as_uint(y);
     const uint32_t sign = (u >> 24) & 0x80u;
     const uint32_t a = u & 0x7FFFFFFFu;
-    if (a > 0x7F800000u) return 0x7Fu;               // NaN
-    if (a >= 0x43E00000u) return sign | 0x7Eu;       // |y| >= 448 (and inf)
-    if (a < 0x3C800000u) {                           // |y| < 2^-6: step 2^-9
-        const float q = __builtin_rintf(__uint_as_float(a) * 512.0f);
-        return sign | (uint32_t)q;                   // q == 8 encodes 2^-6
-    }
-    int32_t e = (int32_t)(a >> 23) - 127;            // -6 .. 8
-    uint32_t mant = a & 0x7FFFFFu;
-    uint32_t r = mant >> 20, rem = mant & 0xFFFFFu;
-    if (rem > 0x80000u || (rem == 0x80000u && (r & 1u))) ++r;
-    if (r == 8u) { r = 0; ++e; }
-    const uint32_t code = ((uint32_t)(e + 7) << 3) | r;
-    return sign | (code > 0x7Eu ? 0x7Eu : code);
+    const uint32_t a_sat = a < 0x43E00000u ? a : 0x43E00000u;            // |y| >= 448, inf -> 448
+    const uint32_t cn = ((a_sat + 0x7FFFFu + ((a_sat >> 20) & 1u)) >> 20) - 960u;
+    const uint32_t cs = (uint32_t)__builtin_rintf(__uint_as_float(a) * 512.0f);
+    const uint32_t code = sign | (a < 0x3C800000u ? cs : (cn < 0x7Eu ? cn : 0x7Eu));
+    return a > 0x7F800000u ? 0x7Fu : code;
+}
+
+// The quotient RN(x / s) that the quantisation takes, for a divisor s shared
+// by a whole (block, head) tile: from r = RN(1 / s), q0 = RN(x r), the exact
+// residual e = x - q0 s (one FMA) and the corrected q1 = RN(q0 + e r)
+// (Markstein's final correction step).  For s in [2^-100, 2^100] this gives
+// the same e4m3 code as the correctly rounded quotient for every finite bf16
+// x (checked exhaustively on the CPU over x and every scale fp32(b / 448), b
+// a positive bf16); quotients past 512 saturate either way and keep q0, and
+// the sign is q0's (a zero x keeps its sign).  Other scales divide.
+struct Recip {
+    float s, r;
+    bool fast;
+};
+__device__ __forceinline__ Recip recip_of(float s) {
+    return {s, 1.0f / s, s >= 0x1p-100f && s <= 0x1p100f};
+}
+__device__ __forceinline__ float quotient(float x, const Recip &d) {
+    if (!d.fast) return x / d.s;
+    const float q0 = x * d.r;
+    const float e = __builtin_fmaf(-q0, d.s, x);
+    const float q1 = __builtin_fmaf(e, d.r, q0);
+    return __builtin_copysignf(__builtin_fabsf(q0) < 512.0f ? q1 : q0, q0);
 }
 
 __device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -145,6 +164,8 @@ __device__ __forceinline__ int block_scan_window(int32_t *cnt, int n, int32_t *w
 // and is written when m_lo <= m < m_hi.  K rows go straight to the pool;
 // V rows are transposed through the wave's LDS tile to [d][16 slots] and
 // written as whole 16-slot rows when the block is full, else slot by slot.
+// e4m3: a block that is not written whole (a decode row's slot) quantises
+// only its written slots, each slot's K and V rows spread over all 64 lanes.
 template <int D, bool FP8>
 __device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, int h, int lane,
                                             uint16_t *tr, int t0, int p0, int L) {
@@ -241,40 +262,56 @@ __device__ __forceinline__ void append_unit(const AppendArgs &a, int r, int j, i
             sk = a.k_scale[si];
             sv = a.v_scale[si];
         }
-        if (mine) {
+        const Recip dk = recip_of(sk), dv = recip_of(sv);
+        if (!full) {
+            // the written slots only, each K row spread over the whole wave
+            // (DPL values per lane), as V below
+#pragma unroll
+            for (int s2 = 0; s2 < 16; ++s2) {
+                if (s2 < m_lo || s2 >= m_hi) continue;
+                const uint16_t *kp = a.k_new + (int64_t)(t0 + sb - p0 + s2) * tok_stride +
+                                     (int64_t)h * D + lane * DPL;
+                const uint32_t w = DPL == 2 ? *(const uint32_t *)kp : (uint32_t)*kp;
+                uint32_t c = 0;
+#pragma unroll
+                for (int e = 0; e < DPL; ++e)
+                    c |= f32_to_e4m3(quotient(bf16_bits_to_f32((w >> (16 * e)) & 0xFFFFu), dk)) << (8 * e);
+                if constexpr (DPL == 2) *(uint16_t *)(kdst + s2 * D + lane * 2) = (uint16_t)c;
+                else kdst[s2 * D + lane] = (uint8_t)c;
+            }
+        } else if (mine) {
             // 8 codes per 16-byte bf16 word
 #pragma unroll
             for (int w = 0; w < QW; ++w) {
                 uint32_t c[2] = {0u, 0u};
 #pragma unroll
                 for (int x = 0; x < 4; ++x) {
-                    const uint32_t lo8 = f32_to_e4m3(bf16_bits_to_f32(kw[w][x] & 0xFFFFu) / sk);
-                    const uint32_t hi8 = f32_to_e4m3(bf16_bits_to_f32(kw[w][x] >> 16) / sk);
+                    const uint32_t lo8 = f32_to_e4m3(quotient(bf16_bits_to_f32(kw[w][x] & 0xFFFFu), dk));
+                    const uint32_t hi8 = f32_to_e4m3(quotient(bf16_bits_to_f32(kw[w][x] >> 16), dk));
                     c[x >> 1] |= (lo8 | (hi8 << 8)) << (16 * (x & 1));
                 }
                 *(u32x2_t *)(kdst + m * D + part * (D / 4) + 8 * w) = (u32x2_t){c[0], c[1]};
             }
         }
+        auto vcode = [&](int s2, int e) -> uint32_t {
+            return f32_to_e4m3(quotient(bf16_bits_to_f32((col[s2] >> (16 * e)) & 0xFFFFu), dv));
+        };
 #pragma unroll
         for (int e = 0; e < DPL; ++e) {
             uint8_t *row = vdst + (lane * DPL + e) * 16;
-            uint32_t code[16];
-#pragma unroll
-            for (int s2 = 0; s2 < 16; ++s2)
-                code[s2] = (s2 >= m_lo && s2 < m_hi)
-                               ? f32_to_e4m3(bf16_bits_to_f32((col[s2] >> (16 * e)) & 0xFFFFu) / sv)
-                               : 0u;
             if (full) {
                 uint32_t pk[4];
 #pragma unroll
                 for (int m2 = 0; m2 < 4; ++m2)
-                    pk[m2] = code[4 * m2] | (code[4 * m2 + 1] << 8) | (code[4 * m2 + 2] << 16) |
-                             (code[4 * m2 + 3] << 24);
+                    pk[m2] = vcode(4 * m2, e) | (vcode(4 * m2 + 1, e) << 8) |
+                             (vcode(4 * m2 + 2, e) << 16) | (vcode(4 * m2 + 3, e) << 24);
                 *(u32x4_t *)row = (u32x4_t){pk[0], pk[1], pk[2], pk[3]};
             } else {
+                // the written slots only (the same for the whole wave): a decode
+                // row's unit quantises one slot, not sixteen
 #pragma unroll
                 for (int s2 = 0; s2 < 16; ++s2)
-                    if (s2 >= m_lo && s2 < m_hi) row[s2] = (uint8_t)code[s2];
+                    if (s2 >= m_lo && s2 < m_hi) row[s2] = (uint8_t)vcode(s2, e);
             }
         }
     }
@@ -399,13 +436,16 @@ __global__ __launch_bounds__(256) void append_rows_kernel(AppendArgs a) {
             sk = a.k_scale[si];
             sv = a.v_scale[si];
         }
+        const Recip dk = recip_of(sk), dv = recip_of(sv);
         for (int i = 0; i < n; ++i) {
             const int slot = (lo + i) & 15;
 #pragma unroll
             for (int e = 0; e < DPL; ++e) {
                 const int d = lane * DPL + e;
-                kdst[slot * D + d] = (uint8_t)f32_to_e4m3(bf16_bits_to_f32(a.k_new[src + i * tok_stride + d]) / sk);
-                vdst[d * 16 + slot] = (uint8_t)f32_to_e4m3(bf16_bits_to_f32(a.v_new[src + i * tok_stride + d]) / sv);
+                kdst[slot * D + d] =
+                    (uint8_t)f32_to_e4m3(quotient(bf16_bits_to_f32(a.k_new[src + i * tok_stride + d]), dk));
+                vdst[d * 16 + slot] =
+                    (uint8_t)f32_to_e4m3(quotient(bf16_bits_to_f32(a.v_new[src + i * tok_stride + d]), dv));
             }
         }
     }
