@@ -145,6 +145,29 @@ def test_fp8_prefill_values_near_the_fp16_range(torch_cuda):
     assert err <= ATOL * f
 
 
+@pytest.mark.parametrize("log2f", [-120, -90, 100, 110])
+def test_fp8_append_scales_at_the_range_edges(torch_cuda, log2f):
+    # The e4m3 append takes x / s from a reciprocal and one correction for
+    # tile scales s in [2^-100, 2^100] and divides outside.  K and V (new and
+    # cached) times 2^log2f put the scales (about amax / 448, amax ~ 3-4 times
+    # the factor) below 2^-100 (a subnormal scale at 2^-120), just inside the
+    # low edge, inside the high edge and above it; codes and scales must equal
+    # the oracle's bit for bit
+    rows = [W.RowSpec(W.PREFILL, 0, 40), W.RowSpec(W.DECODE, 20, 1), W.RowSpec(W.PREFILL, 16, 33),
+            W.RowSpec(W.DECODE, 47, 1)]
+    w = W.build(f"fp8-scale-2^{log2f}", rows, {}, 8, 2, 128, kv_dtype=W.KV_FP8, seed=37)
+    for name in ("k_new", "v_new", "ctx_k", "ctx_v"):
+        setattr(w, name, _bf16_scaled(getattr(w, name), 2.0 ** log2f))
+    it = _run(w, torch_cuda)
+    pool, _ = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    ks = pool.k_scale[pool.k_scale > 0]
+    lo, hi = float(ks.min()), float(ks.max())
+    say(f"[case] fp8 append, K/V x 2^{log2f}: tile scales {lo:.3e} .. {hi:.3e}")
+    fast = (ks >= 2.0 ** -100) & (ks <= 2.0 ** 100)
+    assert fast.all() if log2f in (-90, 100) else not fast.any()
+
+
 def _rows_case(name, n_decode, prefill_q, kv, seed):
     g = np.random.Generator(np.random.PCG64(seed))
     rows = [W.RowSpec(W.DECODE, int(g.integers(0, 80)), 1, int(g.integers(-1, 2)))
