@@ -321,8 +321,15 @@ def measure(cfg, steps, warmup, check_error, threads):
              "kernels_ms": {k: round(v, 4) for k, v in kms.items()}}
     if kms["decode_ms"] > 0:
         gbs = dec_bytes / (kms["decode_ms"] * 1e-3) / 1e9
+        # logical: every decode row's keys counted, shared prefixes included
+        # (the bytes a kernel that reads each row's cache separately would move)
+        dec_rows = w.batch.row_kind == W.DECODE
+        log_bytes = int(w.batch.seq_lens[dec_rows].astype(np.int64).sum()) * Hkv * kv_tok + \
+            n_dec * Hq * D * (2 + 4)
         entry["decode"] = {"GBps": round(gbs, 1), "frac_hbm": round(gbs / HBM_PEAK_GBS, 4),
-                           "algorithmic_bytes": int(dec_bytes), "ms": round(kms["decode_ms"], 4)}
+                           "algorithmic_bytes": int(dec_bytes), "ms": round(kms["decode_ms"], 4),
+                           "logical_GBps": round(log_bytes / (kms["decode_ms"] * 1e-3) / 1e9, 1),
+                           "logical_bytes": int(log_bytes)}
     if kms["prefill_ms"] > 0:
         tf = pf_flops / (kms["prefill_ms"] * 1e-3) / 1e12
         entry["prefill"] = {"TFLOPs": round(tf, 1), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
