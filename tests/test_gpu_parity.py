@@ -476,3 +476,32 @@ def test_host_workspace_must_be_pinned(torch_cuda):
     pool, ref = oracle.run_iteration(w)
     err, _ = attn_error(it.out.cpu().numpy().reshape(ref.shape), ref)
     assert err <= ATOL
+
+
+def _random_batch(k):
+    """Random batch k: GQA group, KV heads, head_dim, cache dtype, row count,
+    context and chunk lengths and prefix groups all drawn (seeded)."""
+    g = np.random.Generator(np.random.PCG64([4242, k]))
+    G = int(g.choice([1, 2, 3, 4, 5, 6, 8, 12, 16, 24, 32]))
+    hkv = int(g.choice([1, 2, 4])) if G <= 16 else int(g.choice([1, 2]))
+    D = int(g.choice([64, 128]))
+    kv = W.KV_FP8 if g.random() < 0.5 else W.KV_BF16
+    return W.random_case(4242 + k, num_rows=int(g.integers(1, 40)), num_q_heads=G * hkv,
+                         num_kv_heads=hkv, head_dim=D, kv_dtype=kv,
+                         max_ctx=int(g.choice([50, 300, 1500, 4000])),
+                         max_q=int(g.choice([1, 20, 100, 400])), n_groups=int(g.integers(0, 4)))
+
+
+@pytest.mark.parametrize("k", range(40))
+def test_random_batches(torch_cuda, k):
+    # forty random batches, host-planned (even k) and device-planned (odd k):
+    # pools bit-exact and every output within the tolerance
+    w = _random_batch(k)
+    mirrors = k % 2 == 0
+    say(f"[case] random batch {k}: rows={w.batch.num_rows} T={w.batch.num_tokens} "
+        f"Hq={w.num_q_heads} Hkv={w.num_kv_heads} D={w.head_dim} kv={w.kv_dtype} mirrors={mirrors}")
+    it = _run(w, torch_cuda, mirrors=mirrors)
+    pool, ref = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    err, _ = attn_error(it.out.cpu().numpy().reshape(ref.shape), ref)
+    assert err <= ATOL
