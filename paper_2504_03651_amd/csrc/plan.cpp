@@ -136,19 +136,38 @@ int build_plan(const HostBatch &b, int32_t Hkv, int32_t Hq, int32_t D, const Pla
     // (piece, KV head, head chunk) units.
     int64_t seg_blocks = 0;
     for (const Segment &s : segs) seg_blocks += s.j1 - s.j0;
-    const int32_t split = (int32_t)std::max<int64_t>(
-        std::min<int32_t>(kMinSplitBlocks, std::max(2, opt.split_blocks)),
-        std::min<int64_t>(opt.split_blocks, seg_blocks * Hkv * nhc / kSplitTargetUnits));
+    const int32_t min_split = std::min<int32_t>(kMinSplitBlocks, std::max(2, opt.split_blocks));
+    const int64_t units_cap = seg_blocks * Hkv * nhc / kSplitTargetUnits;
+    int32_t split = (int32_t)std::max<int64_t>(min_split, std::min<int64_t>(opt.split_blocks, units_cap));
+    auto waves_for = [&](int32_t sp) {
+        int64_t n = 0;
+        for (const Segment &s : segs)
+            n += (int64_t)((s.j1 - s.j0 + sp - 1) / sp) * ((s.nrows + nt_max - 1) / nt_max);
+        return n * plan.waves_per_desc;
+    };
+    // A launch that fits one generation of resident waves starts every wave
+    // at once and has no partly filled last generation: when pieces up to
+    // kOneGenerationStretch times longer (and no longer than the unit target
+    // allows) bring the launch under that, take the shortest such length.
+    const int64_t slots = (int64_t)kDecodeWavesPerCu * opt.num_cus;
+    const int32_t stretch_cap = (int32_t)std::max<int64_t>(
+        split, std::min<int64_t>((int64_t)kOneGenerationStretch * opt.split_blocks, units_cap));
+    if (waves_for(split) > slots && waves_for(stretch_cap) <= slots) {
+        int32_t lo = split + 1, hi = stretch_cap;
+        while (lo < hi) {
+            const int32_t mid = lo + (hi - lo) / 2;
+            if (waves_for(mid) <= slots) hi = mid;
+            else lo = mid + 1;
+        }
+        split = lo;
+    }
 
     // contributions per decode row: sum over its segments of their splits
     std::vector<int32_t> &cnt = plan.cnt, &moff = plan.moff, &cursor = plan.cursor;
     cnt.assign((size_t)B, 0);
     auto n_splits = [&](const Segment &s) { return (s.j1 - s.j0 + split - 1) / split; };
-    int64_t n_waves = 0;
-    for (const Segment &s : segs)
-        n_waves += (int64_t)n_splits(s) * ((s.nrows + nt_max - 1) / nt_max) * plan.waves_per_desc;
-    const bool equal_pieces =
-        n_waves <= (int64_t)kEqualPieceGenerations * kDecodeWavesPerCu * opt.num_cus;
+    const int64_t n_waves = waves_for(split);
+    const bool equal_pieces = n_waves <= (int64_t)kEqualPieceGenerations * slots;
     for (const Segment &s : segs)
         for (int32_t k = 0; k < s.nrows; ++k) cnt[seg_rows[s.rows_off + k]] += n_splits(s);
 

@@ -83,6 +83,15 @@ constexpr int kSplitTargetUnits = 2048;   // decode units below which pieces shr
 // decode-only and e4m3 batches, 4.1 and 3.4 generations, 3-4% slower)
 constexpr int kEqualPieceGenerations = ECHO_EQ_GENS;
 constexpr int kDecodeWavesPerCu = 12;
+#ifndef ECHO_ONE_GEN_STRETCH
+#define ECHO_ONE_GEN_STRETCH 4
+#endif
+// Decode pieces may grow up to this many times the default length when that
+// lets the whole launch fit one generation of resident waves (measured on
+// MI355X: the long-context batch goes from 2.5 generations at 48 blocks to
+// one at 128, decode 0.442 -> 0.386 ms; batches that cannot get there keep
+// the default)
+constexpr int kOneGenerationStretch = ECHO_ONE_GEN_STRETCH;
 
 // Wave w of the attention grid handles descriptor w / (Hkv * head_chunks),
 // KV head (w % (Hkv * head_chunks)) / head_chunks and head chunk

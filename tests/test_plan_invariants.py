@@ -313,3 +313,20 @@ def test_equal_pieces_on_few_generation_launches():
             else:
                 assert all(n == 48 for n in nblk[:-1]), nblk
         assert split_ranges > 10
+
+
+def test_pieces_stretch_to_fit_one_generation():
+    # the long-context batch's decode (28 rows of 32k keys, GQA 64/8) needs
+    # 2.5 generations of resident waves (12 per CU x 256 CUs) at the default
+    # 48-block pieces; pieces of up to 4x that length fit it into one, and the
+    # planner takes the shortest that does (equal lengths, 118-128 blocks).
+    # The mixed batch cannot get under one generation (its ranges are short)
+    # and keeps the default
+    for cfg, longest in ((4, 128), (3, 48), (2, 48)):
+        w = W.config(cfg, values=False)
+        lay, d = _decode_pieces(w)
+        waves = len(d) * w.num_kv_heads * lay["head_chunks"]
+        nblk = (d[:, 4] - d[:, 3] + 15) // 16
+        assert nblk.max() == longest
+        if cfg == 4:   # one generation, and not stretched further than needed
+            assert 0.9 * 12 * 256 < waves <= 12 * 256
