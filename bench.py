@@ -379,8 +379,8 @@ def main():
         return layer_bench(args)
     if args.gpus != 1:
         print(f"bench.py measures one GPU only (asked for --gpus {args.gpus}); the hot path "
-              "shards by KV head or by prefix group with no exchange, but this build runs on a "
-              "single MI355X.", file=sys.stderr)
+              "would shard by KV head or by prefix group with no exchange, but the library "
+              "drives a single MI355X.", file=sys.stderr)
         return 2
     import torch
     from paper_2504_03651_amd import echo
