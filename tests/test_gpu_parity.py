@@ -145,6 +145,29 @@ def test_fp8_prefill_values_near_the_fp16_range(torch_cuda):
     assert err <= ATOL * f
 
 
+LARGE_LOGITS = [
+    # seed, Hq, Hkv, D, kv, query factor
+    (131, 8, 2, 128, W.KV_BF16, 4.0),
+    (132, 8, 2, 128, W.KV_BF16, 16.0),
+    (133, 16, 4, 64, W.KV_BF16, 16.0),
+    (134, 8, 2, 128, W.KV_FP8, 16.0),
+]
+
+
+@pytest.mark.parametrize("case", LARGE_LOGITS, ids=[f"seed{c[0]}-x{int(c[5])}" for c in LARGE_LOGITS])
+def test_large_logits(torch_cuda, case):
+    # Queries times 4 and 16 (exact in bf16): logits 4 and 16 times those of
+    # N(0, 1) data, softmax rows from flat to nearly one-hot.  Scores are
+    # scaled in fp32 after the product, so the error bound does not grow with
+    # the logits' magnitude (rounding q * scale to bf16 first would put up to
+    # 2^-9 |logit| into every exponent: beyond the bar at these sizes).
+    seed, hq, hkv, d, kv, f = case
+    w = W.random_case(seed, num_rows=8, num_q_heads=hq, num_kv_heads=hkv, head_dim=d,
+                      kv_dtype=kv, max_ctx=900, max_q=150, n_groups=2, prefill_frac=0.5)
+    w.q = _bf16_scaled(w.q, f)
+    _check_small(w, torch_cuda, f"large-logits-{seed}-x{f:g}")
+
+
 @pytest.mark.parametrize("log2f", [-120, -90, 100, 110])
 def test_fp8_append_scales_at_the_range_edges(torch_cuda, log2f):
     # The e4m3 append takes x / s from a reciprocal and one correction for
