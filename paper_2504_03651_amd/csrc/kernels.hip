@@ -578,6 +578,16 @@ __device__ __forceinline__ int dec_logical(int P, int run_log2) {
 
 // One decode workgroup of four waves: P is its physical workgroup index in
 // the decode order (dec_logical), tid its thread index in [0, 256).
+// Decode waves are bound by the CU's texture address units, and the SIMD
+// issues the oldest ready wave first, so of three resident waves the oldest
+// streams about twice as fast as the youngest.  Each wave therefore sets its
+// issue priority from the 32-key steps it has left (longest remaining work
+// first), which evens out the end times the planner assumes equal.
+#ifndef ECHO_DEC_PRIO
+#define ECHO_DEC_PRIO 24, 12, 6
+#endif
+constexpr int kDecPrio[3] = {ECHO_DEC_PRIO};   // steps left for priority 3, 2, 1
+
 template <int D, bool FP8>
 __device__ __forceinline__ void decode_body(const AttnArgs &a, int P, int tid) {
     typedef KV<FP8> kv;
@@ -659,6 +669,11 @@ __device__ __forceinline__ void decode_body(const AttnArgs &a, int P, int tid) {
     auto sweep = [&](auto nt_flag) {
         constexpr bool NTL = decltype(nt_flag)::value;
         for (int kb = key_begin; kb < key_end; kb += 32) {
+            const int left = (key_end - kb + 31) >> 5;
+            if (left >= kDecPrio[0]) __builtin_amdgcn_s_setprio(3);
+            else if (left >= kDecPrio[1]) __builtin_amdgcn_s_setprio(2);
+            else if (left >= kDecPrio[2]) __builtin_amdgcn_s_setprio(1);
+            else __builtin_amdgcn_s_setprio(0);
             const int jb = kb >> 4;
             const int b0 = ro_load(btr, jb);
             const bool has1 = kb + 16 < key_end;
