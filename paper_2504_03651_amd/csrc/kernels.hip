@@ -692,6 +692,10 @@ __device__ __forceinline__ void decode_body(const AttnArgs &a, int P, int tid) {
             const KT *vp = vbase + (int64_t)vblk * blk_stride + c16 * 16 + vslot;
 #pragma unroll
             for (int i = 0; i < NT; ++i) vr[i] = pool_load<NTL, VRaw>(vp + i * 256);
+            // every K and V load of the step goes out before the products (left
+            // to itself the compiler reuses K's registers for V and issues the
+            // V loads only after the first K values arrive)
+            __builtin_amdgcn_sched_barrier(0);
 
             f32x4_t s[2];
 #pragma unroll
