@@ -1057,13 +1057,14 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
                     sc[t][nn] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(kf, qf[nn][c], sc[t][nn], 0, 0, 0);
             }
     };
-    const float f = FP8 ? 1.f : scale;  // raw score -> log2 units (e4m3 scales first)
-    // scale (e4m3), mask, and this lane's max over its 8 scores of each query
-    // column in log2 units (the column's max over its 4 lanes is formed only
-    // on the rare rescale path)
-    auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2]) {
-        float sk = scale;
-        if constexpr (FP8) sk = scale * lscale[buf * 4 + 2 * ch + (g4 >> 1)];
+    // mask, and this lane's max over its 8 raw scores of each query column in
+    // log2 units (the column's max over its 4 lanes is formed only on the rare
+    // rescale path); f receives the chunk's raw score -> log2 factor, which for
+    // e4m3 includes the K scale of this lane's block (positive, so the max of
+    // the raw scores gives the max of the scaled ones)
+    auto prep = [&](int buf, int kt, int ch, bool masked, f32x4_t (&sc)[2][2], float (&mc)[2], float &f) {
+        f = scale;
+        if constexpr (FP8) f = scale * lscale[buf * 4 + 2 * ch + (g4 >> 1)];
         const int key0 = kPfKeys * kt + 32 * ch + 8 * g4;
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
@@ -1073,7 +1074,6 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
 #pragma unroll
                 for (int r = 0; r < 4; ++r) {
                     float v = sc[t][nn][r];
-                    if constexpr (FP8) v *= sk;
                     if (masked) v = (key0 + 4 * t + r < klim[nn]) ? v : -INFINITY;
                     sc[t][nn][r] = v;
                     mx = fmaxf(mx, v);
@@ -1095,7 +1095,7 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
         }
     };
     // exponentials of one chunk against m_run, packed to bf16 (fp16 for e4m3)
-    auto expo = [&](const f32x4_t (&sc)[2][2], PT (&pf)[2]) {
+    auto expo = [&](const f32x4_t (&sc)[2][2], PT (&pf)[2], float f) {
 #pragma unroll
         for (int nn = 0; nn < 2; ++nn) {
 #pragma unroll
@@ -1124,18 +1124,18 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
         const uint8_t *kl = lds + buf * LD::STAGE;
         const uint8_t *vl = kl + LD::KBYTES;
         f32x4_t s0[2][2], s1[2][2];
-        float m0[2], m1[2];
+        float m0[2], m1[2], f0, f1;
         PT p0[2], p1[2];
         qk(kl, 0, s0);
-        prep(buf, kt, 0, masked, s0, m0);
+        prep(buf, kt, 0, masked, s0, m0, f0);
         if (__any(m0[0] > m_hig[0] || m0[1] > m_hig[1])) {
             const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m0[0])),
                                  fmaxf(m_run[1], wave_max_xor16_32(m0[1]))};
             rescale(mn);
         }
         qk(kl, 1, s1);          // MFMA ...
-        expo(s0, p0);           // ... with the exponentials of chunk 0
-        prep(buf, kt, 1, masked, s1, m1);
+        expo(s0, p0, f0);       // ... with the exponentials of chunk 0
+        prep(buf, kt, 1, masked, s1, m1, f1);
         if (__any(m1[0] > m_hig[0] || m1[1] > m_hig[1])) {
             // chunk 0's probabilities, not yet added, move with the reference
             const float mn[2] = {fmaxf(m_run[0], wave_max_xor16_32(m1[0])),
@@ -1150,7 +1150,7 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
             rescale(mn);
         }
         pv(vl, 0, p0);          // MFMA ...
-        expo(s1, p1);           // ... with the exponentials of chunk 1
+        expo(s1, p1, f1);       // ... with the exponentials of chunk 1
         pv(vl, 1, p1);
         const float mt[2] = {vmax(m0[0], m1[0]), vmax(m0[1], m1[1])};
         if (__any(mt[0] > m_hi8[0] || mt[1] > m_hi8[1])) {
