@@ -838,6 +838,8 @@ struct PfLds {
 
 // s_waitcnt operand: vmcnt(n) with expcnt and lgkmcnt left free
 constexpr int waitcnt_vm(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8); }
+// vmcnt(n) and lgkmcnt(0): also every LDS write of this wave has landed
+constexpr int waitcnt_vm_lds(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
 typedef __attribute__((address_space(3))) void lds_void_t;
 
@@ -1173,8 +1175,10 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
     store_tile(0);
     if (LA == 2 && ntiles > kt0 + 1) issue_tile(kt0 + 1, 1, tile_id(kt0 + 1));
     int id_ahead = tile_id(kt0 + LA);   // block id of the next tile to issue
+    // (e4m3 tiles reach LDS through ds_write, which the barrier does not wait
+    // for: this wave's writes must have landed before others read them)
     if (LA == 2 && ntiles > kt0 + 1) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
-    else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+    else __builtin_amdgcn_s_waitcnt(FP8 ? waitcnt_vm_lds(0) : waitcnt_vm(0));
     __builtin_amdgcn_s_barrier();
     if (tail_tile == kt0) {
         zero_tail(kt0, 0);
@@ -1193,7 +1197,7 @@ __device__ __forceinline__ void prefill_piece(const PrefillArgs &a, int kvh, int
         if (kt + 1 < ntiles) {
             if constexpr (LA == 1) store_tile((kt + 1 - kt0) % kPfStages);
             if (ahead) __builtin_amdgcn_s_waitcnt(waitcnt_vm(2 * NJ));
-            else __builtin_amdgcn_s_waitcnt(waitcnt_vm(0));
+            else __builtin_amdgcn_s_waitcnt(FP8 ? waitcnt_vm_lds(0) : waitcnt_vm(0));
             __builtin_amdgcn_s_barrier();
             if (kt + 1 == tail_tile) {
                 zero_tail(kt + 1, (kt + 1 - kt0) % kPfStages);
