@@ -145,6 +145,29 @@ def test_fp8_prefill_values_near_the_fp16_range(torch_cuda):
     assert err <= ATOL * f
 
 
+@pytest.mark.parametrize("log2f", [-12, 6])
+def test_fp8_prefill_v_scales(torch_cuda, log2f):
+    # The e4m3 prefill widens V codes with the power-of-two part of the block
+    # scale and multiplies by its mantissa in fp16.  V times 2^-12 and 2^6 (on
+    # N(0, 1) data the scales sit near 2^-7) moves the scales' exponents to
+    # about 2^-19 and 2^-1; outputs scale with V, and so does the bar
+    rows = [W.RowSpec(W.PREFILL, 0, 120), W.RowSpec(W.PREFILL, 200, 64), W.RowSpec(W.DECODE, 300, 1),
+            W.RowSpec(W.PREFILL, 700, 33)]
+    w = W.build(f"fp8-v-2^{log2f}", rows, {}, 16, 4, 128, kv_dtype=W.KV_FP8, seed=41)
+    f = 2.0 ** log2f
+    w.v_new = _bf16_scaled(w.v_new, f)
+    w.ctx_v = _bf16_scaled(w.ctx_v, f)
+    say(f"[case] fp8 prefill with V x 2^{log2f}")
+    it = _run(w, torch_cuda)
+    pool, ref = oracle.run_iteration(w)
+    same_pool(it.pool_host(), pool)
+    got = it.out.cpu().numpy().reshape(ref.shape)
+    assert np.isfinite(got).all()
+    err, nerr = attn_error(got, ref)
+    say(f"       max abs err {err:.3e} (bar {ATOL * f:.3e})  normalised {nerr:.3e}")
+    assert err <= ATOL * f
+
+
 LARGE_LOGITS = [
     # seed, Hq, Hkv, D, kv, query factor
     (131, 8, 2, 128, W.KV_BF16, 4.0),
